@@ -1,0 +1,211 @@
+/*
+ * aep.h -- C ABI of libaep, the MI355X (gfx950) expert-layer hot path of
+ * Asynchronous Expert Parallelism (AEP).
+ *
+ * The calls follow the paper's statement of the problem (Sec. 3.2, execution
+ * engine): a receptor files arriving tokens under a LayerID = (block, expert)
+ * queue (the "mu-queue"); when the GPU is free a scheduler picks a layer
+ * (Sec. 3.4); the executor drains that layer's queues, merges the fragments
+ * into one contiguous batch (re-batching), runs the experts, and the top-K
+ * duplicates of each token are merged back with their gate weights (Sec. 3.2,
+ * "Top-K support").  Token data stays on the GPU; queue metadata that the host
+ * can know without a device sync (token and row totals) is kept on the host.
+ *
+ * Conventions for every entry point:
+ *  - Every call returns an aep_status.  Argument, capacity and state errors
+ *    are detected on the host before anything is launched and leave all state
+ *    unchanged.  Launch failures return AEP_ERR_DEVICE.  Bad values that only
+ *    the device can see (an out-of-range token id, a non-finite logit, two
+ *    rows for one (token, slot)) set a device error flag and are reported as
+ *    AEP_ERR_DEVICE by the next aep_sync; the offending value is clamped so
+ *    that every memory access stays in bounds.  Nothing aborts or throws
+ *    across the ABI.
+ *  - "device pointer" arguments are HIP device allocations owned by the
+ *    caller and only borrowed by the library; "host pointer" arguments are
+ *    ordinary host memory.  All device work of a call is enqueued on the
+ *    given stream (a hipStream_t; NULL is the legacy default stream), in
+ *    stream order, and the call returns without waiting unless stated.
+ *  - One host thread drives a context at a time.  Calls on one context must
+ *    be ordered on one stream (or ordered by the caller across streams).
+ *  - Matrices are row-major with the last dimension contiguous.  Weight
+ *    matrices are stored out x in (the reduction dimension contiguous):
+ *    W_gate, W_up [d_ffn][d_model], W_down [d_model][d_ffn].
+ *  - Element formats: AEP_F32 = IEEE binary32; AEP_BF16 = bfloat16 (upper
+ *    half of a binary32); AEP_FP8_E4M3 = OCP FP8 E4M3 ("e4m3fn": bias 7,
+ *    largest finite 448, S.1111.111 is NaN, no infinities).
+ */
+#ifndef AEP_H_
+#define AEP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AEP_OK = 0,
+  AEP_ERR_INVALID_ARG = 1, /* a NULL/out-of-range argument or bad config      */
+  AEP_ERR_CAPACITY = 2,    /* the queue or workspace cannot hold the request  */
+  AEP_ERR_EMPTY = 3,       /* nothing queued (drain / pick)                   */
+  AEP_ERR_STATE = 4,       /* call out of order (no workspace, stale batch...) */
+  AEP_ERR_DEVICE = 5,      /* HIP error or device-detected bad input          */
+  AEP_ERR_UNSUPPORTED = 6  /* valid but not implemented (shape, dtype combo)  */
+} aep_status;
+
+typedef enum { AEP_F32 = 0, AEP_BF16 = 1, AEP_FP8_E4M3 = 2 } aep_dtype;
+
+/* Layer-pick policies (Sec. 3.4): most-tokens-first-serve, first-layer-first-
+ * serve, and the defragging scheduler (Algorithm 1). */
+typedef enum { AEP_POLICY_MTFS = 0, AEP_POLICY_FLFS = 1, AEP_POLICY_DEFRAG = 2 } aep_policy;
+
+typedef struct {
+  int32_t n_layers;    /* MoE layers (blocks) whose queues live in this context */
+  int32_t n_experts;   /* routed experts per layer, E (routing needs E <= 64)   */
+  int32_t n_shared;    /* shared experts per layer (see every token, weight 1)  */
+  int32_t d_model;     /* d: multiple of 64                                      */
+  int32_t d_ffn;       /* f: multiple of 64                                      */
+  int32_t top_k;       /* k: slots per token, 1 <= k <= min(E, 8)               */
+  int32_t renorm;      /* 1: gate weights renormalised over the k selected      */
+  int32_t act_dtype;   /* aep_dtype of activations, H and outputs: F32 or BF16  */
+  int32_t w_dtype;     /* aep_dtype of weights: F32 (with F32 act), BF16 or      */
+                       /* FP8_E4M3 (with BF16 act)                               */
+  int32_t max_tokens_per_layer; /* queue capacity: tokens a layer may hold     */
+} aep_config;
+
+/* A drained layer.  Filled by aep_rebatch; all pointers are device views into
+ * the bound workspace and stay valid until aep_release_batch (or the next
+ * aep_rebatch, which is refused while a batch is outstanding).
+ *
+ * Row space of the batch: rows [0, n_routed) are the routed rows, experts in
+ * ascending id, each expert's queue in arrival order; when shared experts
+ * exist, shared expert s owns rows [n_routed + s*n_tokens, ... + n_tokens),
+ * one per token in id order.  n_rows = n_routed + n_shared * n_tokens. */
+typedef struct {
+  int32_t layer;
+  int32_t n_tokens;          /* tokens of the layer (rows of the combine output)  */
+  int64_t n_routed;          /* routed rows, sum of counts[0..E)                   */
+  int64_t n_rows;            /* rows of y (routed + shared)                        */
+  uint64_t epoch;            /* identifies the batch; stale handles are refused    */
+  const void* x_perm;        /* [n_routed (+ n_tokens if shared)][d] act dtype:    */
+                             /*   routed rows, then every token in id order       */
+  const int32_t* counts;     /* [E + n_shared] rows per group                      */
+  const int32_t* offsets;    /* [E + n_shared + 1] first row of each group         */
+  const int32_t* row_token;  /* [n_routed] token id of each routed row             */
+  const float* row_weight;   /* [n_routed] gate weight of each routed row          */
+  const int32_t* token_pos;  /* [n_tokens][k] row of (token, slot), -1 if absent   */
+  const float* token_weight; /* [n_tokens][k] gate weight of (token, slot), 0 if absent */
+} aep_batch;
+
+/* Human-readable name of a status (static string, never NULL). */
+const char* aep_status_string(aep_status s);
+
+/* Create a context for cfg (copied).  Validates the configuration; allocates
+ * host state only.  *out receives the handle.  No device work. */
+aep_status aep_create(const aep_config* cfg, void** out);
+
+/* Destroy a context (NULL is allowed).  Does not free the caller's workspace. */
+aep_status aep_destroy(void* ctx);
+
+/* Bytes of device workspace this configuration needs (host only). */
+aep_status aep_workspace_size(const void* ctx, size_t* bytes);
+
+/* Bind a caller-allocated device workspace of at least aep_workspace_size
+ * bytes, 256-byte aligned, on the current HIP device.  Initialises it on
+ * `stream` and waits for that.  Resets every queue.  The workspace holds the
+ * mu-queues, weight tables, the batch buffers and the FFN intermediate. */
+aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream);
+
+/* Register one expert's weights for a layer (pointers are borrowed and must
+ * stay valid while the layer can run).  expert in [0, E) is routed; expert
+ * in [E, E + n_shared) is shared expert expert - E.  Device pointers:
+ *   w_gate, w_up [d_ffn][d_model], w_down [d_model][d_ffn] in w_dtype;
+ *   for FP8 weights, scale_gate_up [2 * d_ffn] (gate channels, then up
+ *   channels) and scale_down [d_model], bf16: W = code * scale per output
+ *   channel.  Scales must be NULL for other weight types.
+ * Copies the pointer table to the device on `stream` and waits for it. */
+aep_status aep_set_expert_weights(void* ctx, int32_t layer, int32_t expert, const void* w_gate,
+                                  const void* w_up, const void* w_down, const void* scale_gate_up,
+                                  const void* scale_down, void* stream);
+
+/* Receptor + router for one arriving fragment of T tokens (Sec. 3.2):
+ * routes each token on its gate logits (device, f32 [T][E]; top-k by logit,
+ * larger first, equal logits -> lower expert id; weights = softmax
+ * probabilities of the k selected, renormalised when cfg.renorm) and appends
+ * one queue entry per (token, slot) to queue (layer, expert), in (token,
+ * slot) order.  x (device, [T][d] act dtype) is NOT copied: entries refer to
+ * its rows, so it must stay valid until this layer's aep_rebatch has run on
+ * the stream.  Tokens get layer-local ids continuing the layer's count.
+ * idx_out [T][k] int32 and w_out [T][k] f32 (device, may be NULL) receive
+ * the routing.  T == 0 is a no-op.  AEP_ERR_CAPACITY if the layer could
+ * exceed max_tokens_per_layer. */
+aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
+                             int32_t* idx_out, float* w_out, void* stream);
+
+/* Receptor for rows routed elsewhere: appends n rows to queue (layer,
+ * expert) in order.  Device pointers: rows [n][d] act dtype (referenced,
+ * not copied, as above), token_ids [n] int32 in [0, n_tokens), slots [n]
+ * int32 in [0, k) (NULL: all 0), gate_w [n] f32.  The layer's token count
+ * becomes max(current, n_tokens).  Not available on layers with shared
+ * experts (AEP_ERR_UNSUPPORTED).  n == 0 is a no-op. */
+aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void* rows,
+                            const int32_t* token_ids, const int32_t* slots, const float* gate_w,
+                            int32_t n, int32_t n_tokens, void* stream);
+
+/* Host-side queue totals of a layer (no device access). */
+aep_status aep_queue_depth(const void* ctx, int32_t layer, int64_t* tokens, int64_t* rows);
+
+/* Per-expert queue depths of a layer copied to host memory h_counts [E];
+ * synchronises `stream`. */
+aep_status aep_expert_counts(void* ctx, int32_t layer, int32_t* h_counts, void* stream);
+
+/* Scheduler (Sec. 3.4): pick the next layer to drain from the host-side
+ * queue totals.  MTFS: most queued rows (ties: lowest layer).  FLFS: lowest
+ * non-empty layer.  DEFRAG: Algorithm 1 at layer granularity, score(b) =
+ * rows(b) + sum_{i=1..lookahead} rows((b+i) mod n_layers) * delta^i, over
+ * non-empty layers (ties: lowest).  AEP_ERR_EMPTY when nothing is queued. */
+aep_status aep_pick_layer(const void* ctx, int32_t policy, double delta, int32_t lookahead,
+                          int32_t* layer);
+
+/* Executor, re-batch (Sec. 3.2): drain every queue of `layer` into one
+ * contiguous batch -- per-expert counts and offsets, then a gather of every
+ * queued row into x_perm (a bit copy) -- and empty the layer's queues.  Fills
+ * *out (host struct).  AEP_ERR_EMPTY if nothing is queued, AEP_ERR_STATE if
+ * a batch is still outstanding or weights of the layer are missing. */
+aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream);
+
+/* Expert FFN of a batch: every group g computes, on its rows,
+ * y = W_down (silu(W_gate x) * (W_up x)), silu(v) = v / (1 + e^-v), with
+ * f32 accumulation; the intermediate h is rounded to the act dtype.
+ * y: device [n_rows][d] act dtype, caller-owned. */
+aep_status aep_expert_ffn(void* ctx, const aep_batch* batch, void* y, void* stream);
+
+/* The two halves of aep_expert_ffn, for callers that schedule (or time) them
+ * separately.  aep_expert_gate_up computes h = silu(W_gate x) * (W_up x) for
+ * every row of the batch into the workspace; aep_expert_down then computes
+ * y = W_down h.  aep_expert_down must follow aep_expert_gate_up of the same
+ * batch in stream order (the library does not check this). */
+aep_status aep_expert_gate_up(void* ctx, const aep_batch* batch, void* stream);
+aep_status aep_expert_down(void* ctx, const aep_batch* batch, void* y, void* stream);
+
+/* Top-K merge (Sec. 3.2): out[t] = sum_{j<k} token_weight[t][j] *
+ * y[token_pos[t][j]] (slots ascending, absent slots skipped) + sum_s
+ * y[n_routed + s*n_tokens + t], accumulated in f32 and rounded once.
+ * out: device [n_tokens][d] act dtype, caller-owned. */
+aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* out, void* stream);
+
+/* Release a batch; its buffers may then be reused by the next aep_rebatch. */
+aep_status aep_release_batch(void* ctx, aep_batch* batch);
+
+/* Wait for `stream`, then report (and clear) the device error flag. */
+aep_status aep_sync(void* ctx, void* stream);
+
+/* Utility: decode n OCP e4m3fn codes (device) to bf16 (device); exact. */
+aep_status aep_fp8_e4m3_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AEP_H_ */

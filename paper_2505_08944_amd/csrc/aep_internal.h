@@ -1,0 +1,98 @@
+// Internal definitions shared by libaep's host code and its gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace aep {
+
+// One mu-queue entry (16 bytes): the row it refers to (the token's tensor
+// stays where it arrived, as the paper's token metadata refers to GPU-resident
+// input tensors), the layer-local token id and top-k slot, and the gate weight.
+struct QEntry {
+  const void* row;
+  int32_t token_slot;  // token | slot << 24
+  float w;
+};
+static_assert(sizeof(QEntry) == 16, "QEntry must be 16 bytes");
+
+constexpr int kTokenBits = 24;
+constexpr int32_t kTokenMask = (1 << kTokenBits) - 1;
+
+// Weights of one expert (device pointers) -- the per-layer table the FFN
+// kernels read.
+struct WeightDesc {
+  const void* gate;
+  const void* up;
+  const void* down;
+  const uint16_t* s_gu;    // fp8 only: [2f] bf16 scales
+  const uint16_t* s_down;  // fp8 only: [d]  bf16 scales
+  const void* pad;
+};
+static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
+
+// One FFN group of a drained batch, written by the plan kernel.
+struct GroupDesc {
+  int32_t n;       // rows
+  int32_t x_row0;  // first row in x_perm
+  int32_t y_row0;  // first row in h and y
+  int32_t bm;      // row-tile height used for this group
+  int32_t tile0_gu;  // first gate/up tile of the group
+  int32_t tile0_dn;  // first down tile of the group
+  int32_t mt;        // row tiles
+  int32_t pad;
+};
+static_assert(sizeof(GroupDesc) == 32, "GroupDesc layout");
+
+// Device error flag bits.
+constexpr int32_t kErrNonFinite = 1;
+constexpr int32_t kErrTokenRange = 2;
+constexpr int32_t kErrSlotRange = 4;
+constexpr int32_t kErrCollision = 8;
+
+constexpr int kRouteThreads = 256;
+constexpr int kMaxRouteExperts = 64;
+constexpr int kMaxTopK = 8;
+constexpr int kMaxGroups = 1024;
+
+// FFN tiling (bf16 / fp8 weights): tiles of BM rows x BN columns; gate/up
+// tiles cover BN/2 features of gate and the same BN/2 of up.
+constexpr int kBM = 256;
+constexpr int kBN = 256;
+constexpr int kBK = 64;
+// f32 path
+constexpr int kBM32 = 64;
+constexpr int kBN32 = 64;
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipGetLastError() after the launch.
+hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,
+                        float* r_w, int32_t* r_rank, int32_t* blockcnt, int32_t* idx_out,
+                        float* w_out, int32_t* err, hipStream_t s);
+hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* r_rank,
+                         const int32_t* blockcnt, int T, int E, int k, const char* x,
+                         int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
+                         int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
+                         hipStream_t s);
+hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_t* token_ids,
+                               const int32_t* slots, const float* gate_w, int n, int n_tokens,
+                               int k, int expert, int E, const int32_t* depth_cur,
+                               int32_t* depth_nxt, QEntry* q, int64_t q_stride, int32_t* err,
+                               hipStream_t s);
+hipError_t launch_plan(int E, int S, int n_tokens, int k, int32_t* depth, int32_t* counts,
+                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, int nt_gu,
+                       int nt_dn, int bm, int32_t* pos, float* posw, hipStream_t s);
+hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,
+                         int64_t N, int n_tokens, int shared, const void* const* tok_row,
+                         char* xp, int64_t row_bytes, int32_t* row_token, float* row_w,
+                         int32_t* pos, float* posw, int k, int32_t* err, hipStream_t s);
+// stage 0: gate/up (xp -> h), stage 1: down (h -> y); max_tiles bounds the
+// stage's tile count (the exact count is on the device).
+hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
+                      const WeightDesc* wtab, int G, const int32_t* tile_totals, int max_tiles,
+                      const void* xp, void* h, void* y, int d, int f, int num_cu, hipStream_t s);
+hipError_t launch_combine(int act_dtype, const void* y, int64_t N, int n_tokens, int S, int k,
+                          const int32_t* pos, const float* posw, void* out, int d, hipStream_t s);
+hipError_t launch_fp8_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, hipStream_t s);
+
+}  // namespace aep

@@ -1,0 +1,502 @@
+// libaep host side: the C ABI declared in include/aep.h.
+//
+// Host state per layer holds what the host can know without a device sync --
+// tokens and rows queued, an upper bound of every expert's queue depth (for
+// capacity checks), which half of the device depth ping-pong is current --
+// while the queue entries themselves, the per-expert depths and everything
+// derived from them live in the caller's device workspace.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "aep.h"
+#include "aep_internal.h"
+
+using namespace aep;
+
+namespace {
+
+struct LayerState {
+  int32_t tokens = 0;         // layer-local token ids handed out / declared
+  int64_t rows = 0;           // queued rows
+  int64_t routed_tokens = 0;  // tokens that came through the router
+  std::vector<int64_t> explicit_rows;  // per expert, rows from aep_enqueue_rows
+  int cur = 0;                         // current half of the depth ping-pong
+  std::vector<uint8_t> have_w;         // weights registered, per group
+};
+
+struct Ctx {
+  aep_config cfg{};
+  int G = 0;
+  int esz = 0;  // bytes per activation element
+  // workspace layout (byte offsets)
+  size_t off_err = 0, off_depth = 0, off_q = 0, off_tokrow = 0, off_wtab = 0;
+  size_t off_ridx = 0, off_rw = 0, off_rrank = 0, off_blockcnt = 0;
+  size_t off_counts = 0, off_offsets = 0, off_groups = 0, off_tiles = 0;
+  size_t off_xp = 0, off_rowtok = 0, off_roww = 0, off_pos = 0, off_posw = 0, off_h = 0;
+  size_t ws_need = 0;
+  char* ws = nullptr;
+  int device = -1;
+  int num_cu = 0;
+  std::vector<LayerState> layers;
+  std::vector<WeightDesc> wtab_host;  // [layer][group]
+  bool batch_out = false;
+  uint64_t epoch = 0;
+  int32_t batch_layer = -1;
+
+  int64_t tmax() const { return cfg.max_tokens_per_layer; }
+  int64_t row_cap() const { return tmax() * cfg.top_k; }
+  int32_t* err() const { return reinterpret_cast<int32_t*>(ws + off_err); }
+  int32_t* depth(int layer, int half) const {
+    return reinterpret_cast<int32_t*>(ws + off_depth) + ((int64_t)layer * 2 + half) * cfg.n_experts;
+  }
+  QEntry* q(int layer) const {
+    return reinterpret_cast<QEntry*>(ws + off_q) + (int64_t)layer * cfg.n_experts * tmax();
+  }
+  const void** tokrow(int layer) const {
+    return reinterpret_cast<const void**>(ws + off_tokrow) + (int64_t)layer * tmax();
+  }
+  WeightDesc* wtab(int layer) const {
+    return reinterpret_cast<WeightDesc*>(ws + off_wtab) + (int64_t)layer * G;
+  }
+  template <typename T>
+  T* at(size_t off) const {
+    return reinterpret_cast<T*>(ws + off);
+  }
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool layout(Ctx& c) {
+  const aep_config& g = c.cfg;
+  const int64_t L = g.n_layers, E = g.n_experts, S = g.n_shared, T = g.max_tokens_per_layer,
+                k = g.top_k, d = g.d_model, f = g.d_ffn;
+  const int64_t N = T * k;
+  const int64_t xrows = N + (S ? T : 0);
+  const int64_t hrows = N + S * T;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align256(o + bytes);
+    return at;
+  };
+  c.off_err = take(256);
+  c.off_depth = take(sizeof(int32_t) * L * 2 * E);
+  c.off_q = take(sizeof(QEntry) * L * E * T);
+  c.off_tokrow = take(sizeof(void*) * L * T);
+  c.off_wtab = take(sizeof(WeightDesc) * L * c.G);
+  c.off_ridx = take(sizeof(int32_t) * N);
+  c.off_rw = take(sizeof(float) * N);
+  c.off_rrank = take(sizeof(int32_t) * N);
+  c.off_blockcnt = take(sizeof(int32_t) * ((T + kRouteThreads - 1) / kRouteThreads) * E);
+  c.off_counts = take(sizeof(int32_t) * c.G);
+  c.off_offsets = take(sizeof(int32_t) * (c.G + 1));
+  c.off_groups = take(sizeof(GroupDesc) * c.G);
+  c.off_tiles = take(sizeof(int32_t) * 2);
+  c.off_xp = take((size_t)xrows * d * c.esz);
+  c.off_rowtok = take(sizeof(int32_t) * N);
+  c.off_roww = take(sizeof(float) * N);
+  c.off_pos = take(sizeof(int32_t) * N);
+  c.off_posw = take(sizeof(float) * N);
+  c.off_h = take((size_t)hrows * f * c.esz);
+  c.ws_need = o;
+  return true;
+}
+
+Ctx* as_ctx(void* p) { return reinterpret_cast<Ctx*>(p); }
+const Ctx* as_ctx(const void* p) { return reinterpret_cast<const Ctx*>(p); }
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE; }
+
+// column tiles and row-tile height of the FFN launches
+void tiling(const Ctx& c, int* nt_gu, int* nt_dn, int* bm) {
+  const int d = c.cfg.d_model, f = c.cfg.d_ffn;
+  if (c.cfg.act_dtype == AEP_F32) {
+    *nt_gu = (f + kBN32 - 1) / kBN32;
+    *nt_dn = (d + kBN32 - 1) / kBN32;
+    *bm = kBM32;
+  } else {
+    *nt_gu = (f + kBN / 2 - 1) / (kBN / 2);
+    *nt_dn = (d + kBN - 1) / kBN;
+    *bm = kBM;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* aep_status_string(aep_status s) {
+  switch (s) {
+    case AEP_OK: return "AEP_OK";
+    case AEP_ERR_INVALID_ARG: return "AEP_ERR_INVALID_ARG";
+    case AEP_ERR_CAPACITY: return "AEP_ERR_CAPACITY";
+    case AEP_ERR_EMPTY: return "AEP_ERR_EMPTY";
+    case AEP_ERR_STATE: return "AEP_ERR_STATE";
+    case AEP_ERR_DEVICE: return "AEP_ERR_DEVICE";
+    case AEP_ERR_UNSUPPORTED: return "AEP_ERR_UNSUPPORTED";
+  }
+  return "AEP_ERR_UNKNOWN";
+}
+
+aep_status aep_create(const aep_config* cfg, void** out) {
+  if (!cfg || !out) return AEP_ERR_INVALID_ARG;
+  const aep_config& g = *cfg;
+  if (g.n_layers < 1 || g.n_experts < 1 || g.n_shared < 0 ||
+      g.n_experts + g.n_shared > kMaxGroups)
+    return AEP_ERR_INVALID_ARG;
+  if (g.d_model < 64 || g.d_ffn < 64 || g.d_model % 64 || g.d_ffn % 64) return AEP_ERR_UNSUPPORTED;
+  if (g.top_k < 1 || g.top_k > g.n_experts || g.top_k > kMaxTopK) return AEP_ERR_INVALID_ARG;
+  if (g.renorm != 0 && g.renorm != 1) return AEP_ERR_INVALID_ARG;
+  if (g.max_tokens_per_layer < 1 || g.max_tokens_per_layer > kTokenMask) return AEP_ERR_INVALID_ARG;
+  const bool f32 = g.act_dtype == AEP_F32 && g.w_dtype == AEP_F32;
+  const bool bf = g.act_dtype == AEP_BF16 && (g.w_dtype == AEP_BF16 || g.w_dtype == AEP_FP8_E4M3);
+  if (!f32 && !bf) {
+    const bool known = (g.act_dtype >= 0 && g.act_dtype <= 2) && (g.w_dtype >= 0 && g.w_dtype <= 2);
+    return known ? AEP_ERR_UNSUPPORTED : AEP_ERR_INVALID_ARG;
+  }
+  Ctx* c = new (std::nothrow) Ctx();
+  if (!c) return AEP_ERR_CAPACITY;
+  c->cfg = g;
+  c->G = g.n_experts + g.n_shared;
+  c->esz = g.act_dtype == AEP_F32 ? 4 : 2;
+  layout(*c);
+  c->layers.resize(g.n_layers);
+  for (auto& l : c->layers) {
+    l.explicit_rows.assign(g.n_experts, 0);
+    l.have_w.assign(c->G, 0);
+  }
+  c->wtab_host.assign((size_t)g.n_layers * c->G, WeightDesc{});
+  *out = c;
+  return AEP_OK;
+}
+
+aep_status aep_destroy(void* ctx) {
+  delete as_ctx(ctx);
+  return AEP_OK;
+}
+
+aep_status aep_workspace_size(const void* ctx, size_t* bytes) {
+  if (!ctx || !bytes) return AEP_ERR_INVALID_ARG;
+  *bytes = as_ctx(ctx)->ws_need;
+  return AEP_OK;
+}
+
+aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !d_ws) return AEP_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(d_ws) & 255) return AEP_ERR_INVALID_ARG;
+  if (bytes < c->ws_need) return AEP_ERR_CAPACITY;
+  if (c->batch_out) return AEP_ERR_STATE;
+  int devid = -1, ncu = 0;
+  if (hipGetDevice(&devid) != hipSuccess) return AEP_ERR_DEVICE;
+  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, devid) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  hipStream_t s = as_stream(stream);
+  char* ws = reinterpret_cast<char*>(d_ws);
+  // clear the error flag, every depth counter and the weight tables
+  if (hipMemsetAsync(ws + c->off_err, 0, c->off_q - c->off_err, s) != hipSuccess) return AEP_ERR_DEVICE;
+  if (hipMemsetAsync(ws + c->off_wtab, 0, sizeof(WeightDesc) * c->cfg.n_layers * c->G, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  if (hipStreamSynchronize(s) != hipSuccess) return AEP_ERR_DEVICE;
+  c->ws = ws;
+  c->device = devid;
+  c->num_cu = ncu > 0 ? ncu : 1;
+  for (auto& l : c->layers) {
+    l.tokens = 0;
+    l.rows = 0;
+    l.routed_tokens = 0;
+    l.cur = 0;
+    std::fill(l.explicit_rows.begin(), l.explicit_rows.end(), 0);
+    std::fill(l.have_w.begin(), l.have_w.end(), 0);
+  }
+  std::fill(c->wtab_host.begin(), c->wtab_host.end(), WeightDesc{});
+  return AEP_OK;
+}
+
+aep_status aep_set_expert_weights(void* ctx, int32_t layer, int32_t expert, const void* w_gate,
+                                  const void* w_up, const void* w_down, const void* scale_gate_up,
+                                  const void* scale_down, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return AEP_ERR_INVALID_ARG;
+  if (!c->ws) return AEP_ERR_STATE;
+  if (layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->G) return AEP_ERR_INVALID_ARG;
+  if (!w_gate || !w_up || !w_down) return AEP_ERR_INVALID_ARG;
+  const bool fp8 = c->cfg.w_dtype == AEP_FP8_E4M3;
+  if (fp8 != (scale_gate_up != nullptr) || fp8 != (scale_down != nullptr)) return AEP_ERR_INVALID_ARG;
+  WeightDesc& w = c->wtab_host[(size_t)layer * c->G + expert];
+  w.gate = w_gate;
+  w.up = w_up;
+  w.down = w_down;
+  w.s_gu = reinterpret_cast<const uint16_t*>(scale_gate_up);
+  w.s_down = reinterpret_cast<const uint16_t*>(scale_down);
+  w.pad = nullptr;
+  hipStream_t s = as_stream(stream);
+  if (hipMemcpyAsync(c->wtab(layer) + expert, &w, sizeof(WeightDesc), hipMemcpyHostToDevice, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  if (hipStreamSynchronize(s) != hipSuccess) return AEP_ERR_DEVICE;
+  c->layers[layer].have_w[expert] = 1;
+  return AEP_OK;
+}
+
+aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
+                             int32_t* idx_out, float* w_out, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return AEP_ERR_INVALID_ARG;
+  if (!c->ws) return AEP_ERR_STATE;
+  if (layer < 0 || layer >= c->cfg.n_layers || T < 0) return AEP_ERR_INVALID_ARG;
+  if (T == 0) return AEP_OK;
+  if (!x || !logits) return AEP_ERR_INVALID_ARG;
+  const int E = c->cfg.n_experts, k = c->cfg.top_k;
+  if (E > kMaxRouteExperts) return AEP_ERR_UNSUPPORTED;
+  LayerState& L = c->layers[layer];
+  int64_t ub = 0;
+  for (int e = 0; e < E; ++e) ub = std::max(ub, L.routed_tokens + L.explicit_rows[e]);
+  if ((int64_t)L.tokens + T > c->tmax() || ub + T > c->tmax() || L.rows + (int64_t)T * k > c->row_cap())
+    return AEP_ERR_CAPACITY;
+  hipStream_t s = as_stream(stream);
+  int32_t* ridx = c->at<int32_t>(c->off_ridx);
+  float* rw = c->at<float>(c->off_rw);
+  int32_t* rrank = c->at<int32_t>(c->off_rrank);
+  int32_t* bcnt = c->at<int32_t>(c->off_blockcnt);
+  hipError_t e1 = launch_route(logits, T, E, k, c->cfg.renorm, ridx, rw, rrank, bcnt, idx_out, w_out,
+                               c->err(), s);
+  if (e1 != hipSuccess) return AEP_ERR_DEVICE;
+  const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
+  hipError_t e2 = launch_append(ridx, rw, rrank, bcnt, T, E, k, reinterpret_cast<const char*>(x), row_bytes,
+                                L.tokens, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), c->q(layer),
+                                c->tmax(), c->tokrow(layer), s);
+  if (e2 != hipSuccess) return AEP_ERR_DEVICE;
+  L.cur ^= 1;
+  L.tokens += T;
+  L.rows += (int64_t)T * k;
+  L.routed_tokens += T;
+  return AEP_OK;
+}
+
+aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void* rows,
+                            const int32_t* token_ids, const int32_t* slots, const float* gate_w,
+                            int32_t n, int32_t n_tokens, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return AEP_ERR_INVALID_ARG;
+  if (!c->ws) return AEP_ERR_STATE;
+  if (layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->cfg.n_experts || n < 0)
+    return AEP_ERR_INVALID_ARG;
+  if (c->cfg.n_shared > 0) return AEP_ERR_UNSUPPORTED;
+  if (n == 0) return AEP_OK;
+  if (!rows || !token_ids || !gate_w || n_tokens < 1) return AEP_ERR_INVALID_ARG;
+  LayerState& L = c->layers[layer];
+  if ((int64_t)n_tokens > c->tmax() || L.routed_tokens + L.explicit_rows[expert] + n > c->tmax() ||
+      L.rows + n > c->row_cap())
+    return AEP_ERR_CAPACITY;
+  hipStream_t s = as_stream(stream);
+  const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
+  hipError_t e = launch_enqueue_rows(reinterpret_cast<const char*>(rows), row_bytes, token_ids, slots,
+                                     gate_w, n, n_tokens, c->cfg.top_k, expert, c->cfg.n_experts,
+                                     c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), c->q(layer),
+                                     c->tmax(), c->err(), s);
+  if (e != hipSuccess) return AEP_ERR_DEVICE;
+  L.cur ^= 1;
+  L.tokens = std::max(L.tokens, n_tokens);
+  L.rows += n;
+  L.explicit_rows[expert] += n;
+  return AEP_OK;
+}
+
+aep_status aep_queue_depth(const void* ctx, int32_t layer, int64_t* tokens, int64_t* rows) {
+  const Ctx* c = as_ctx(ctx);
+  if (!c || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
+  if (tokens) *tokens = c->layers[layer].tokens;
+  if (rows) *rows = c->layers[layer].rows;
+  return AEP_OK;
+}
+
+aep_status aep_expert_counts(void* ctx, int32_t layer, int32_t* h_counts, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !h_counts || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
+  if (!c->ws) return AEP_ERR_STATE;
+  hipStream_t s = as_stream(stream);
+  if (hipMemcpyAsync(h_counts, c->depth(layer, c->layers[layer].cur), sizeof(int32_t) * c->cfg.n_experts,
+                     hipMemcpyDeviceToHost, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  return dev(hipStreamSynchronize(s));
+}
+
+aep_status aep_pick_layer(const void* ctx, int32_t policy, double delta, int32_t lookahead,
+                          int32_t* layer) {
+  const Ctx* c = as_ctx(ctx);
+  if (!c || !layer) return AEP_ERR_INVALID_ARG;
+  const int NB = c->cfg.n_layers;
+  bool any = false;
+  for (const auto& l : c->layers) any = any || l.rows > 0;
+  if (policy == AEP_POLICY_MTFS) {
+    if (!any) return AEP_ERR_EMPTY;
+    int best = -1;
+    for (int b = 0; b < NB; ++b)
+      if (c->layers[b].rows > 0 && (best < 0 || c->layers[b].rows > c->layers[best].rows)) best = b;
+    *layer = best;
+    return AEP_OK;
+  }
+  if (policy == AEP_POLICY_FLFS) {
+    if (!any) return AEP_ERR_EMPTY;
+    for (int b = 0; b < NB; ++b)
+      if (c->layers[b].rows > 0) {
+        *layer = b;
+        return AEP_OK;
+      }
+    return AEP_ERR_EMPTY;
+  }
+  if (policy == AEP_POLICY_DEFRAG) {
+    if (lookahead < 0 || !(delta >= 0.0) || !std::isfinite(delta)) return AEP_ERR_INVALID_ARG;
+    if (!any) return AEP_ERR_EMPTY;
+    int best = -1;
+    double best_s = 0.0;
+    for (int b = 0; b < NB; ++b) {
+      if (c->layers[b].rows <= 0) continue;
+      double ls = 0.0, pw = 1.0;
+      for (int i = 1; i <= lookahead; ++i) {
+        pw *= delta;
+        ls += (double)c->layers[(b + i) % NB].rows * pw;
+      }
+      const double sc = ls + (double)c->layers[b].rows;
+      if (best < 0 || sc > best_s) {
+        best = b;
+        best_s = sc;
+      }
+    }
+    *layer = best;
+    return AEP_OK;
+  }
+  return AEP_ERR_INVALID_ARG;
+}
+
+aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !out || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
+  if (!c->ws || c->batch_out) return AEP_ERR_STATE;
+  LayerState& L = c->layers[layer];
+  if (L.rows == 0 && !(c->cfg.n_shared > 0 && L.tokens > 0)) return AEP_ERR_EMPTY;
+  for (int g = 0; g < c->G; ++g)
+    if (!L.have_w[g]) return AEP_ERR_STATE;
+  int nt_gu, nt_dn, bm;
+  tiling(*c, &nt_gu, &nt_dn, &bm);
+  hipStream_t s = as_stream(stream);
+  const int E = c->cfg.n_experts, S = c->cfg.n_shared, k = c->cfg.top_k;
+  int32_t* counts = c->at<int32_t>(c->off_counts);
+  int32_t* offsets = c->at<int32_t>(c->off_offsets);
+  int32_t* pos = c->at<int32_t>(c->off_pos);
+  float* posw = c->at<float>(c->off_posw);
+  if (launch_plan(E, S, L.tokens, k, c->depth(layer, L.cur), counts, offsets, c->at<GroupDesc>(c->off_groups),
+                  c->at<int32_t>(c->off_tiles), nt_gu, nt_dn, bm, pos, posw, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
+  if (launch_gather(c->q(layer), c->tmax(), offsets, E, L.rows, L.tokens, S > 0, c->tokrow(layer),
+                    c->at<char>(c->off_xp), row_bytes, c->at<int32_t>(c->off_rowtok), c->at<float>(c->off_roww),
+                    pos, posw, k, c->err(), s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  c->epoch += 1;
+  c->batch_out = true;
+  c->batch_layer = layer;
+  out->layer = layer;
+  out->n_tokens = L.tokens;
+  out->n_routed = L.rows;
+  out->n_rows = L.rows + (int64_t)S * L.tokens;
+  out->epoch = c->epoch;
+  out->x_perm = c->ws + c->off_xp;
+  out->counts = counts;
+  out->offsets = offsets;
+  out->row_token = c->at<int32_t>(c->off_rowtok);
+  out->row_weight = c->at<float>(c->off_roww);
+  out->token_pos = pos;
+  out->token_weight = posw;
+  L.tokens = 0;
+  L.rows = 0;
+  L.routed_tokens = 0;
+  std::fill(L.explicit_rows.begin(), L.explicit_rows.end(), 0);
+  return AEP_OK;
+}
+
+static aep_status check_batch(const Ctx* c, const aep_batch* b) {
+  if (!c || !b) return AEP_ERR_INVALID_ARG;
+  if (!c->batch_out || b->epoch != c->epoch || b->layer != c->batch_layer) return AEP_ERR_STATE;
+  return AEP_OK;
+}
+
+static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, void* stream) {
+  aep_status st = check_batch(c, batch);
+  if (st != AEP_OK) return st;
+  if (stage == 1 && !y) return AEP_ERR_INVALID_ARG;
+  int nt_gu, nt_dn, bm;
+  tiling(*c, &nt_gu, &nt_dn, &bm);
+  const int64_t E = c->cfg.n_experts, S = c->cfg.n_shared;
+  const int64_t N = batch->n_routed, T = batch->n_tokens;
+  const int64_t row_tiles = N / bm + std::min<int64_t>(E, N) + S * ((T + bm - 1) / bm);
+  const int64_t mt = row_tiles * (stage == 0 ? nt_gu : nt_dn);
+  if (mt > INT32_MAX) return AEP_ERR_UNSUPPORTED;
+  return dev(launch_ffn(stage, c->cfg.act_dtype, c->cfg.w_dtype, c->at<GroupDesc>(c->off_groups),
+                        c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles), (int)mt,
+                        c->ws + c->off_xp, c->ws + c->off_h, y, c->cfg.d_model, c->cfg.d_ffn, c->num_cu,
+                        as_stream(stream)));
+}
+
+aep_status aep_expert_gate_up(void* ctx, const aep_batch* batch, void* stream) {
+  return ffn_stage(as_ctx(ctx), batch, 0, nullptr, stream);
+}
+
+aep_status aep_expert_down(void* ctx, const aep_batch* batch, void* y, void* stream) {
+  return ffn_stage(as_ctx(ctx), batch, 1, y, stream);
+}
+
+aep_status aep_expert_ffn(void* ctx, const aep_batch* batch, void* y, void* stream) {
+  if (!y) return check_batch(as_ctx(ctx), batch) == AEP_OK ? AEP_ERR_INVALID_ARG : check_batch(as_ctx(ctx), batch);
+  aep_status st = ffn_stage(as_ctx(ctx), batch, 0, nullptr, stream);
+  if (st != AEP_OK) return st;
+  return ffn_stage(as_ctx(ctx), batch, 1, y, stream);
+}
+
+aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* out, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  aep_status st = check_batch(c, batch);
+  if (st != AEP_OK) return st;
+  if (!y || !out) return AEP_ERR_INVALID_ARG;
+  return dev(launch_combine(c->cfg.act_dtype, y, batch->n_routed, batch->n_tokens, c->cfg.n_shared,
+                            c->cfg.top_k, batch->token_pos, batch->token_weight, out, c->cfg.d_model,
+                            as_stream(stream)));
+}
+
+aep_status aep_release_batch(void* ctx, aep_batch* batch) {
+  Ctx* c = as_ctx(ctx);
+  aep_status st = check_batch(c, batch);
+  if (st != AEP_OK) return st;
+  c->batch_out = false;
+  c->batch_layer = -1;
+  std::memset(batch, 0, sizeof(*batch));
+  return AEP_OK;
+}
+
+aep_status aep_sync(void* ctx, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return AEP_ERR_INVALID_ARG;
+  if (!c->ws) return AEP_ERR_STATE;
+  if (hipStreamSynchronize(as_stream(stream)) != hipSuccess) return AEP_ERR_DEVICE;
+  int32_t flag = 0;
+  if (hipMemcpy(&flag, c->err(), sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess) return AEP_ERR_DEVICE;
+  if (flag != 0) {
+    const int32_t zero = 0;
+    if (hipMemcpy(c->err(), &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return AEP_ERR_DEVICE;
+    return AEP_ERR_DEVICE;
+  }
+  return AEP_OK;
+}
+
+aep_status aep_fp8_e4m3_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stream) {
+  if (n < 0) return AEP_ERR_INVALID_ARG;
+  if (n == 0) return AEP_OK;
+  if (!codes || !out) return AEP_ERR_INVALID_ARG;
+  return dev(launch_fp8_to_bf16(codes, out, n, as_stream(stream)));
+}
+
+}  // extern "C"

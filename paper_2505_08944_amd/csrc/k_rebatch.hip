@@ -1,0 +1,129 @@
+// Executor re-batch kernels: drain plan + gather.
+//
+// plan (one workgroup): reads the drained layer's per-expert queue depths,
+// writes counts / exclusive-scan offsets / the FFN group table (row bases and
+// tile ranges), resets the queue depths to zero and clears the (token, slot)
+// -> row map.
+//
+// gather: one wave per batch row.  A routed row finds its expert by binary
+// search over the offsets, reads its queue entry and copies the referenced
+// row (16-byte vector loads/stores, the whole wave on one row, so each row is
+// one contiguous coalesced stream); lane 0 records the row's token and gate
+// weight and the (token, slot) -> row map.  Shared-expert rows copy every
+// token's row in id order.
+#include "aep_internal.h"
+
+namespace aep {
+
+__global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, int k,
+                                                    int32_t* __restrict__ depth,
+                                                    int32_t* __restrict__ counts,
+                                                    int32_t* __restrict__ offsets,
+                                                    GroupDesc* __restrict__ groups,
+                                                    int32_t* __restrict__ tile_totals, int nt_gu,
+                                                    int nt_dn, int bm, int32_t* __restrict__ pos,
+                                                    float* __restrict__ posw) {
+  __shared__ int32_t cnt[kMaxGroups];
+  const int tid = threadIdx.x;
+  const int G = E + S;
+  for (int g = tid; g < G; g += blockDim.x) cnt[g] = g < E ? depth[g] : n_tokens;
+  __syncthreads();
+  if (tid == 0) {
+    int N = 0;
+    for (int g = 0; g < E; ++g) N += cnt[g];
+    int off = 0, tg = 0, td = 0;
+    for (int g = 0; g < G; ++g) {
+      const int n = cnt[g];
+      const int mt = (n + bm - 1) / bm;
+      GroupDesc gd;
+      gd.n = n;
+      gd.x_row0 = g < E ? off : N;
+      gd.y_row0 = off;
+      gd.bm = bm;
+      gd.tile0_gu = tg;
+      gd.tile0_dn = td;
+      gd.mt = mt;
+      gd.pad = 0;
+      groups[g] = gd;
+      counts[g] = n;
+      offsets[g] = off;
+      off += n;
+      tg += mt * nt_gu;
+      td += mt * nt_dn;
+    }
+    offsets[G] = off;
+    tile_totals[0] = tg;
+    tile_totals[1] = td;
+  }
+  for (int e = tid; e < E; e += blockDim.x) depth[e] = 0;  // the layer's queues are drained
+  const int64_t nk = (int64_t)n_tokens * k;
+  for (int64_t i = tid; i < nk; i += blockDim.x) {
+    pos[i] = -1;
+    posw[i] = 0.f;
+  }
+}
+
+__global__ __launch_bounds__(256) void gather_kernel(
+    const QEntry* __restrict__ q, int64_t q_stride, const int32_t* __restrict__ offsets, int E,
+    int64_t N, int n_tokens, int shared, const void* const* __restrict__ tok_row, char* xp,
+    int64_t row_bytes, int32_t* __restrict__ row_token, float* __restrict__ row_w,
+    int32_t* __restrict__ pos, float* __restrict__ posw, int k, int32_t* __restrict__ err) {
+  __shared__ int32_t off_s[kMaxGroups + 1];
+  for (int i = threadIdx.x; i <= E; i += blockDim.x) off_s[i] = offsets[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t R = N + (shared ? n_tokens : 0);
+  if (r >= R) return;
+  const uint4* src;
+  if (r < N) {
+    int lo = 0, hi = E;  // off_s[lo] <= r < off_s[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (off_s[mid] <= r)
+        lo = mid;
+      else
+        hi = mid;
+    }
+    const QEntry en = q[(int64_t)lo * q_stride + (r - off_s[lo])];
+    src = reinterpret_cast<const uint4*>(en.row);
+    if (lane == 0) {
+      const int tok = en.token_slot & kTokenMask;
+      const int slot = (int)((uint32_t)en.token_slot >> kTokenBits);
+      row_token[r] = tok;
+      row_w[r] = en.w;
+      const int64_t pi = (int64_t)tok * k + slot;
+      const int old = atomicExch(&pos[pi], (int)r);
+      posw[pi] = en.w;
+      if (old != -1) atomicOr(err, kErrCollision);
+    }
+  } else {
+    src = reinterpret_cast<const uint4*>(tok_row[r - N]);
+  }
+  uint4* dst = reinterpret_cast<uint4*>(xp + r * row_bytes);
+  const int nchunk = (int)(row_bytes >> 4);
+#pragma unroll 8
+  for (int c = lane; c < nchunk; c += 64) dst[c] = src[c];
+}
+
+hipError_t launch_plan(int E, int S, int n_tokens, int k, int32_t* depth, int32_t* counts,
+                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, int nt_gu,
+                       int nt_dn, int bm, int32_t* pos, float* posw, hipStream_t s) {
+  plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, depth, counts, offsets, groups, tile_totals,
+                                  nt_gu, nt_dn, bm, pos, posw);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,
+                         int64_t N, int n_tokens, int shared, const void* const* tok_row,
+                         char* xp, int64_t row_bytes, int32_t* row_token, float* row_w,
+                         int32_t* pos, float* posw, int k, int32_t* err, hipStream_t s) {
+  const int64_t R = N + (shared ? n_tokens : 0);
+  if (R == 0) return hipSuccess;
+  const int64_t nb = (R + 3) / 4;
+  gather_kernel<<<(unsigned)nb, 256, 0, s>>>(q, q_stride, offsets, E, N, n_tokens, shared, tok_row,
+                                             xp, row_bytes, row_token, row_w, pos, posw, k, err);
+  return hipGetLastError();
+}
+
+}  // namespace aep
