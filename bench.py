@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""Benchmark of the AEP expert-layer hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+four arriving fragments are routed and appended to the layer's mu-queues,
+the layer is drained (re-batch + gather), the grouped SwiGLU experts run
+(gate/up launch, down launch) and the top-k combine writes the output.
+Inputs and weights are resident in HBM before the timed region starts.
+
+Default workload: a Mixtral-8x7B-style MoE layer in bf16 -- 4096 queued
+tokens, d = 4096, ffn = 14336, 8 experts, top-2, Zipf(1.2) expert skew,
+arriving as 4 fragments.
+
+Prints ONE JSON line (rank 0, N = 1).  Besides the throughput it reports the
+roofline position of the dominant kernel (the gate/up launch, timed with HIP
+events on the stream it runs on) and the CPU oracle timed on a bounded
+sample of the same workload on this host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+METRIC = "expert-layer tokens/sec + % MFMA peak (hot) / % HBM BW (cold), Zipf-skewed"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2", help="synth workload name (routed mode)")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=2048,
+                    help="tokens of the workload the CPU oracle is timed on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1),
+                    help="host threads for input generation")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        sys.stderr.write("bench.py measures one GPU: this build has no multi-GPU path (expert-parallel "
+                         "sharding is described in DESIGN.md); run with --gpus 1.\n")
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2505_08944_amd as aep
+
+    w = synth.workload(args.workload)
+    assert w.mode == "routed" and w.n_layers == 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    # ---------------------------------------------------------------- inputs
+    t_gen = time.perf_counter()
+    frags = synth.layer_fragments(w, 0)
+    ws = synth.all_expert_weights(w, 0, threads=args.threads)
+    act = torch.bfloat16 if w.act == "bf16" else torch.float32
+
+    def dev_t(a, fmt):
+        a = np.ascontiguousarray(a)
+        if fmt == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        if fmt == "fp8":
+            return torch.from_numpy(a).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    xs = [dev_t(f["x"], w.act) for f in frags]
+    lgs = [dev_t(f["logits"], "f32") for f in frags]
+    T = sum(x.shape[0] for x in xs)
+    ctx = aep.Context(1, w.E, w.d, w.f, w.k, n_shared=w.S, renorm=w.renorm, act=w.act, wdt=w.wdt,
+                      max_tokens_per_layer=T)
+    wfmt = "f32" if w.wdt == "f32" else ("fp8" if w.wdt == "fp8" else "bf16")
+    wdev = []
+    for e, ex in enumerate(ws):
+        tens = [dev_t(ex[k], wfmt) for k in ("gate", "up", "down")]
+        sc = [dev_t(ex["gate_up_scale"], "bf16"), dev_t(ex["down_scale"], "bf16")] if w.wdt == "fp8" else [None, None]
+        ctx.set_expert_weights(0, e, *tens, *sc)
+        wdev.append(tens + sc)
+    del ws
+    t_gen = time.perf_counter() - t_gen
+    N_routed = T * w.k
+    n_rows = N_routed + w.S * T
+    y = torch.empty((n_rows, w.d), dtype=act, device=dev)
+    out = torch.empty((T, w.d), dtype=act, device=dev)
+
+    # ---------------------------------------------------------------- step
+    def step(evs=None):
+        if evs:
+            evs[0].record()
+        for x, lg in zip(xs, lgs):
+            ctx.route_enqueue(0, x, lg)
+        if evs:
+            evs[1].record()
+        b = ctx.rebatch(0)
+        if evs:
+            evs[2].record()
+        ctx.expert_gate_up(b)
+        if evs:
+            evs[3].record()
+        ctx.expert_down(b, y)
+        if evs:
+            evs[4].record()
+        ctx.combine(b, y, out)
+        if evs:
+            evs[5].record()
+        ctx.release(b)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.sync()
+    counts = None
+    # expert counts of this workload (outside the timed region)
+    for x, lg in zip(xs, lgs):
+        ctx.route_enqueue(0, x, lg)
+    counts = ctx.expert_counts(0).tolist()
+    b = ctx.rebatch(0)
+    ctx.release(b)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(events[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ctx.sync()  # device error flag must be clear
+
+    stage_names = ["route_enqueue", "rebatch", "gate_up", "down", "combine"]
+    stage_ms = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(K)]))
+                for j, n in enumerate(stage_names)}
+    ms_per_step = elapsed * 1e3 / K
+    tokens_per_s = T * K / elapsed
+
+    # dominant kernel: the gate/up launch (2/3 of the FFN flops)
+    gu_flops = 4.0 * w.d * w.f * n_rows          # two GEMMs of 2*d*f flops per row
+    ffn_flops = 6.0 * w.d * w.f * n_rows
+    gu_s = stage_ms["gate_up"] / 1e3
+    achieved = gu_flops / gu_s / 1e12
+    ffn_s = (stage_ms["gate_up"] + stage_ms["down"]) / 1e3
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": "ffn_mfma_kernel<gated> (gate/up launch)",
+                "per_launch": {"flops": gu_flops, "rows": n_rows, "flops_per_row": 4 * w.d * w.f,
+                               "avg_ms": round(stage_ms["gate_up"], 4)}}
+
+    res = {
+        "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16" if w.act == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.description or w.name, "tokens": T, "d_model": w.d, "d_ffn": w.f,
+                   "experts": w.E, "shared_experts": w.S, "top_k": w.k, "zipf_s": w.zipf_s,
+                   "fragments": len(xs), "weights": w.wdt, "expert_counts": counts},
+        "roofline": roofline,
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "ffn": {"tflops": round(ffn_flops / ffn_s / 1e12, 2),
+                "mfma_frac": round(ffn_flops / ffn_s / 1e12 / PEAK_BF16_TFLOPS, 4)},
+        "setup_s": round(t_gen, 1),
+    }
+
+    # ---------------------------------------------------------------- CPU oracle
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
+
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(w, n_tok: int):
+    """The oracle, as it stands, on the first n_tok tokens of the workload."""
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = None
+    frags = synth.layer_fragments(w, 0)
+    x = np.concatenate([f["x"] for f in frags])[:n_tok]
+    lg = np.concatenate([f["logits"] for f in frags])[:n_tok]
+    ws = synth.all_expert_weights(w, 0, threads=min(16, os.cpu_count() or 1))
+    t0 = time.perf_counter()
+    lq = oracle.LayerQueues(w.E, w.k, w.S, w.renorm)
+    lq.enqueue_routed(x, lg)
+    oracle.moe_layer(lq, ws, w.act, "f32" if w.wdt == "f32" else w.wdt)
+    dt = time.perf_counter() - t0
+    cpu = platform.processor() or platform.machine()
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(n_tok / dt, 2), "unit": "tokens/s", "cores": blas_threads, "kind": "oracle",
+            "sample": f"first {n_tok} of {sum(w.tokens)} tokens, whole layer (route, queue, re-batch, "
+                      f"float64 SwiGLU experts, combine); {dt:.1f} s",
+            "host_cpu": cpu, "host_logical_cpus": os.cpu_count()}
+
+
+if __name__ == "__main__":
+    main()
