@@ -15,15 +15,16 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-// OCP e4m3fn code -> bf16 bits, exact: normal codes move the exponent (bias
-// 7 -> 127) and the mantissa (3 -> 7 bits); subnormal codes m * 2^-9 go
-// through an exact f32 product; S.1111.111 becomes a quiet NaN.
-__device__ __forceinline__ uint32_t e4m3_to_bf16_bits(uint32_t b) {
-  const uint32_t sgn = (b & 0x80u) << 8;
-  const uint32_t em = b & 0x7fu;
-  if (em == 0x7fu) return sgn | 0x7fc0u;
-  if (em >= 8u) return sgn | ((em + (120u << 3)) << 4);
-  return sgn | (__float_as_uint((float)em * 0x1p-9f) >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Four OCP e4m3fn codes (one 32-bit word, lowest byte first) -> four bf16
+// (two words, lowest first).  gfx950's fp8 conversions use the OCP e4m3fn
+// encoding; with a scale of 1 the conversion is exact (every e4m3 value is a
+// bf16 value).
+__device__ __forceinline__ uint2 e4m3x4_to_bf16x4(uint32_t w) {
+  const bf16x2_t lo = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false);
+  const bf16x2_t hi = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true);
+  return make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
 }  // namespace aep

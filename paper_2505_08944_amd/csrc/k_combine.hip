@@ -83,8 +83,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
 
 __global__ void fp8_to_bf16_kernel(const uint8_t* __restrict__ in, uint16_t* __restrict__ out,
                                    int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) out[i] = (uint16_t)e4m3_to_bf16_bits(in[i]);
+  const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;  // four codes per thread
+  if (i0 >= n) return;
+  const int m = n - i0 < 4 ? (int)(n - i0) : 4;
+  uint32_t w = 0;
+  for (int j = 0; j < m; ++j) w |= (uint32_t)in[i0 + j] << (8 * j);
+  const uint2 v = e4m3x4_to_bf16x4(w);
+  const uint16_t h[4] = {(uint16_t)v.x, (uint16_t)(v.x >> 16), (uint16_t)v.y, (uint16_t)(v.y >> 16)};
+  for (int j = 0; j < m; ++j) out[i0 + j] = h[j];
 }
 
 hipError_t launch_combine(int act_dtype, const void* y, int64_t N, int n_tokens, int S, int k,
@@ -100,7 +106,7 @@ hipError_t launch_combine(int act_dtype, const void* y, int64_t N, int n_tokens,
 
 hipError_t launch_fp8_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  const int64_t nb = (n + 255) / 256;
+  const int64_t nb = ((n + 3) / 4 + 255) / 256;
   fp8_to_bf16_kernel<<<(unsigned)nb, 256, 0, s>>>(codes, out, n);
   return hipGetLastError();
 }

@@ -81,13 +81,12 @@ __device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
   return lo;
 }
 
-__device__ __forceinline__ uint4 widen_fp8_lo(uint4 v) {  // bytes 0..7 -> 8 bf16
-  uint4 o;
-  o.x = e4m3_to_bf16_bits(v.x & 0xff) | (e4m3_to_bf16_bits((v.x >> 8) & 0xff) << 16);
-  o.y = e4m3_to_bf16_bits((v.x >> 16) & 0xff) | (e4m3_to_bf16_bits(v.x >> 24) << 16);
-  o.z = e4m3_to_bf16_bits(v.y & 0xff) | (e4m3_to_bf16_bits((v.y >> 8) & 0xff) << 16);
-  o.w = e4m3_to_bf16_bits((v.y >> 16) & 0xff) | (e4m3_to_bf16_bits(v.y >> 24) << 16);
-  return o;
+// 16 fp8 codes -> 16 bf16 (two 16-byte chunks, lowest k first)
+__device__ __forceinline__ void widen_fp8(uint4 v, uint4& lo, uint4& hi) {
+  const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
+  const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
+  lo = make_uint4(a.x, a.y, b.x, b.y);
+  hi = make_uint4(c.x, c.y, d.x, d.y);
 }
 
 constexpr int kStage = (kBM + kBN) * kLds;  // bf16 elements per LDS stage (A tile then B tile)
@@ -153,37 +152,38 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
       boff[i] = FP8 ? (uint32_t)(c * K + (tid & 3) * 16) : (uint32_t)(c * K + (tid & 7) * 8);
     }
 
-    uint4 ra[8], rb[kBChunks];
-#define AEP_GLOAD(kt)                                                                            \
+    // Two register sets of global-load staging: the loads of step kt + 2
+    // are issued at the start of step kt, so every load has a full K step to
+    // arrive before its data is written to LDS during step kt + 1.
+    uint4 ra0[8], rb0[kBChunks], ra1[8], rb1[kBChunks];
+#define AEP_GLOAD(RA, RB, kt)                                                                    \
   do {                                                                                           \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) ra[i] = gload16(abase + aoff[i] + (kt) * kBK); \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) RA[i] = gload16(abase + aoff[i] + (kt) * kBK); \
     _Pragma("unroll") for (int i = 0; i < kBChunks; ++i) {                                       \
       const bool up_ = GATED && (FP8 ? (i & 1) : ((i >> 1) & 1));                                \
-      rb[i] = gload16((up_ ? bup : bgate) + ((size_t)boff[i] + (size_t)(kt) * kBK) * (FP8 ? 1 : 2)); \
+      RB[i] = gload16((up_ ? bup : bgate) + ((size_t)boff[i] + (size_t)(kt) * kBK) * (FP8 ? 1 : 2)); \
     }                                                                                            \
   } while (0)
-#define AEP_LSTORE(st)                                                                           \
+#define AEP_LSTORE(RA, RB, st)                                                                   \
   do {                                                                                           \
     uint16_t* As_ = smem + (st) * kStage;                                                        \
     uint16_t* Bs_ = As_ + kBM * kLds;                                                            \
     _Pragma("unroll") for (int i = 0; i < 8; ++i)                                                \
-        *reinterpret_cast<uint4*>(&As_[((tid >> 3) + 32 * i) * kLds + (tid & 7) * 8]) = ra[i];    \
+        *reinterpret_cast<uint4*>(&As_[((tid >> 3) + 32 * i) * kLds + (tid & 7) * 8]) = RA[i];    \
     if constexpr (FP8) {                                                                         \
       _Pragma("unroll") for (int i = 0; i < kBChunks; ++i) {                                     \
         uint16_t* dst_ = &Bs_[((tid >> 2) + 64 * i) * kLds + (tid & 3) * 16];                    \
-        uint4 hi_;                                                                               \
-        hi_.x = rb[i].z;                                                                         \
-        hi_.y = rb[i].w;                                                                         \
-        hi_.z = 0;                                                                               \
-        hi_.w = 0;                                                                               \
-        *reinterpret_cast<uint4*>(dst_) = widen_fp8_lo(rb[i]);                                   \
-        *reinterpret_cast<uint4*>(dst_ + 8) = widen_fp8_lo(hi_);                                 \
+        uint4 lo_, hi_;                                                                          \
+        widen_fp8(RB[i], lo_, hi_);                                                              \
+        *reinterpret_cast<uint4*>(dst_) = lo_;                                                   \
+        *reinterpret_cast<uint4*>(dst_ + 8) = hi_;                                               \
       }                                                                                          \
     } else {                                                                                     \
       _Pragma("unroll") for (int i = 0; i < kBChunks; ++i)                                       \
-          *reinterpret_cast<uint4*>(&Bs_[((tid >> 3) + 32 * i) * kLds + (tid & 7) * 8]) = rb[i];  \
+          *reinterpret_cast<uint4*>(&Bs_[((tid >> 3) + 32 * i) * kLds + (tid & 7) * 8]) = RB[i];  \
     }                                                                                            \
   } while (0)
+  constexpr int kStores = 8 + (FP8 ? 2 * kBChunks : kBChunks);  // LDS writes per thread per step
 
     f32x16_t acc[4][4];
 #pragma unroll
@@ -193,38 +193,105 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    AEP_GLOAD(0);
+#define AEP_READ(Abuf, ks_, A_, B_)                                                              \
+  do {                                                                                           \
+    const uint16_t* As_ = (Abuf);                                                                \
+    const uint16_t* Bs_ = As_ + kBM * kLds;                                                      \
+    const int kof_ = (ks_) * 16 + (lane >> 5) * 8;                                               \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) A_[i] =                                        \
+        *reinterpret_cast<const bf16x8_t*>(&As_[(wm * 128 + i * 32 + (lane & 31)) * kLds + kof_]); \
+    _Pragma("unroll") for (int j = 0; j < 4; ++j) B_[j] =                                        \
+        *reinterpret_cast<const bf16x8_t*>(&Bs_[(wn * 128 + j * 32 + (lane & 31)) * kLds + kof_]); \
+  } while (0)
+#define AEP_MMA(A_, B_)                                                                          \
+  do {                                                                                           \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) _Pragma("unroll") for (int j = 0; j < 4; ++j)  \
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i], B_[j], acc[i][j], 0, 0, 0);   \
+  } while (0)
+// One software-pipeline group: read the operands of the next 16-wide k slice
+// (8 LDS reads) while the 16 MFMAs of the current slice run.  Reads are
+// spread two per four MFMAs: bunching them costs MFMA issue slots (measured
+// on gfx950: 8 reads then 16 MFMAs runs ~10% slower than 2 : 4).
+#define AEP_GROUP(Abuf, ks_, An, Bn, Ac, Bc)                                                     \
+  do {                                                                                           \
+    AEP_READ(Abuf, ks_, An, Bn);                                                                 \
+    AEP_MMA(Ac, Bc);                                                                             \
+    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                         \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+  } while (0)
+// The same, with the global loads of step kt + 2 spread between the MFMAs.
+#define AEP_GROUP_LD(Abuf, ks_, An, Bn, Ac, Bc, RA, RB, kl)                                      \
+  do {                                                                                           \
+    AEP_GLOAD(RA, RB, kl);                                                                       \
+    AEP_READ(Abuf, ks_, An, Bn);                                                                 \
+    AEP_MMA(Ac, Bc);                                                                             \
+    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
+      __builtin_amdgcn_sched_group_barrier(0x020, (8 + kBChunks) / 4, 0);                        \
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                         \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+  } while (0)
+// The same, with the LDS writes of the next step's tile spread between the MFMAs.
+#define AEP_GROUP_ST(Abuf, ks_, An, Bn, Ac, Bc, RA, RB, st)                                      \
+  do {                                                                                           \
+    AEP_READ(Abuf, ks_, An, Bn);                                                                 \
+    AEP_LSTORE(RA, RB, st);                                                                      \
+    AEP_MMA(Ac, Bc);                                                                             \
+    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+  } while (0)
+// One K step (64 deep = four 16-wide slices) over LDS stage kt & 1:
+//   issue the global loads of step kt + 2; slice 0 runs while slice 1 is
+//   read; slice 1 runs while slice 2 is read and the tile of step kt + 1
+//   (loaded during step kt - 1) is written to the other LDS stage; slice 2
+//   runs while slice 3 is read; barrier; slice 3 runs while slice 0 of the
+//   next stage is read.  The other stage was last read during step kt - 1,
+//   before that step's barrier.  Past the last step, loads and stores repeat
+//   the last step's data (kept unconditional so they stay in registers).
+#define AEP_STEP(kt_, RLa, RLb, RSa, RSb)                                                        \
+  do {                                                                                           \
+    const uint16_t* cur_ = smem + ((kt_) & 1) * kStage;                                          \
+    const uint16_t* nxt_ = smem + (((kt_) + 1) & 1) * kStage;                                    \
+    AEP_GROUP_LD(cur_, 1, a1, b1, a0, b0, RLa, RLb, min((kt_) + 2, KT - 1));                     \
+    AEP_GROUP_ST(cur_, 2, a0, b0, a1, b1, RSa, RSb, ((kt_) + 1) & 1);                            \
+    AEP_GROUP(cur_, 3, a1, b1, a0, b0);                                                          \
+    __syncthreads();                                                                             \
+    AEP_GROUP(nxt_, 0, a0, b0, a1, b1);                                                          \
+  } while (0)
+
+    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    AEP_GLOAD(ra0, rb0, 0);
+    AEP_GLOAD(ra1, rb1, min(1, KT - 1));
     __syncthreads();  // every wave is done with the previous tile's LDS
-    AEP_LSTORE(0);
+    AEP_LSTORE(ra0, rb0, 0);
     __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-      // Prefetch of step kt + 1 (the last step reloads itself: the loads and
-      // the LDS store stay unconditional, which keeps them in registers).
-      const int kn = min(kt + 1, KT - 1);
-      AEP_GLOAD(kn);
-      const uint16_t* As = smem + (kt & 1) * kStage;
-      const uint16_t* Bs = As + kBM * kLds;
-#pragma unroll
-      for (int ks = 0; ks < kBK / 16; ++ks) {
-        bf16x8_t a[4], b[4];
-        const int kof = ks * 16 + (lane >> 5) * 8;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          a[i] = *reinterpret_cast<const bf16x8_t*>(&As[(wm * 128 + i * 32 + (lane & 31)) * kLds + kof]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          b[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[(wn * 128 + j * 32 + (lane & 31)) * kLds + kof]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      }
-      // The other stage was last read in step kt - 1, which every wave
-      // finished before the barrier that ended that step.
-      AEP_LSTORE((kt + 1) & 1);
-      __syncthreads();
+    AEP_READ(smem, 0, a0, b0);
+    int kt = 0;
+    for (; kt + 1 < KT; kt += 2) {
+      AEP_STEP(kt, ra0, rb0, ra1, rb1);
+      AEP_STEP(kt + 1, ra1, rb1, ra0, rb0);
     }
+    if (kt < KT) AEP_STEP(kt, ra0, rb0, ra1, rb1);
+#undef AEP_STEP
+#undef AEP_GROUP_ST
+#undef AEP_GROUP_LD
+#undef AEP_GROUP
+#undef AEP_MMA
+#undef AEP_READ
 #undef AEP_GLOAD
 #undef AEP_LSTORE
 
@@ -261,7 +328,7 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
             if constexpr (GATED) {
               const float gv = acc[i][j][r] * sg;
               const float uv = acc[i][j + 2][r] * su;
-              v = gv / (1.f + __expf(-gv)) * uv;
+              v = __fdividef(gv, 1.f + __expf(-gv)) * uv;
             } else {
               v = acc[i][j][r] * sg;
             }
@@ -282,6 +349,234 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
           col = nti * (kBN / 2) + c16 * 8;
         else
           col = nti * kBN + (c16 >> 3) * 128 + pass * 64 + (c16 & 7) * 8;
+        if (row < gd.n && col < n_out) {
+          const uint4 v = *reinterpret_cast<const uint4*>(&Cs[rl * kEpiLd + c16 * 8]);
+          *reinterpret_cast<uint4*>(O + (int64_t)(gd.y_row0 + row) * n_out + col) = v;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------- bf16 weights: direct-to-LDS
+// The same 256 x 256 tiles and quadrant MFMA work, but tiles move from global
+// memory straight into LDS (global_load_lds_dwordx4: 64 lanes x 16 bytes into
+// 1 KB of consecutive LDS, no staging registers), through a ring of STAGES
+// LDS buffers with a prefetch distance of STAGES - 1 K steps of BKS.  LDS
+// rows are not padded; a 16-byte chunk c of tile row r sits at position
+// c ^ s(r), where s spreads the 8 rows read together by one fragment read
+// over distinct banks (s(r) = r % 8 for 128-byte rows, (r / 2) % 4 for
+// 64-byte rows).  Each lane picks the global chunk that belongs at its fixed
+// LDS position, so the swizzle costs nothing at load time.
+#ifndef AEP_DL_BK
+#define AEP_DL_BK 64
+#endif
+#ifndef AEP_DL_STAGES
+#define AEP_DL_STAGES 2
+#endif
+typedef __attribute__((address_space(3))) void* lds_vptr;
+typedef const __attribute__((address_space(1))) void* glb_vptr;
+
+// One direct global -> LDS load: 64 lanes x 16 bytes to lds_addr + 16 * lane.
+// Issued through inline asm so that the compiler does not see an LDS write
+// it cannot disambiguate (it would otherwise wait for every outstanding load
+// before each LDS read); the kernel orders these loads itself with
+// wait_vmcnt + barriers.  M0 holds the LDS destination.
+__device__ __forceinline__ void dload16(const void* gptr, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr),
+               "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+               : "memory", "m0");
+}
+
+// s_waitcnt with only vmcnt constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+template <bool GATED, int BKS, int STAGES>
+__global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
+  constexpr int kRowB = BKS * 2;         // bytes of one tile row per K step
+  constexpr int kCPR = BKS / 8;          // 16-byte chunks per row
+  constexpr int kRPI = 1024 / kRowB;     // rows per direct-load instruction
+  constexpr int kNI = kBM / kRPI / 4;    // direct loads per wave per operand per K step
+  constexpr int kTileB = kBM * kRowB;    // bytes of one operand tile per K step
+  constexpr int kStageB = 2 * kTileB;
+  constexpr int kSlices = BKS / 16;
+  constexpr int kDist = STAGES - 1;
+  static_assert(kBM == kBN, "square tiles");
+  static_assert(STAGES * kStageB >= kBM * kEpiLd * 2, "epilogue staging must fit");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * kStageB];
+  __shared__ int32_t t0s[kMaxGroups + 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int G = p.G;
+  const int total = p.tile_totals[GATED ? 0 : 1];
+  for (int g = tid; g < G; g += 256) t0s[g] = GATED ? p.groups[g].tile0_gu : p.groups[g].tile0_dn;
+  if (tid == 0) t0s[G] = total;
+  __syncthreads();
+
+  const int nwg = gridDim.x;
+  const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
+  const int K = p.K, KT = K / BKS, n_out = p.n_out;
+  const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
+  uint16_t* O = reinterpret_cast<uint16_t*>(p.out);
+
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
+  // loader lane constants: row within an instruction's block, LDS position,
+  // and the k chunk that belongs there
+  const int ld_row = lane / kCPR;
+  const int ld_c = (lane % kCPR) ^ (kCPR == 8 ? (lane >> 3) : ((lane >> 3) & 3));
+  // reader lane constants: fragment row and its swizzle
+  const int rd_row = lane & 31;
+  const int rd_s = kCPR == 8 ? (rd_row & 7) : ((rd_row >> 1) & 3);
+
+  for (int tile = slot; tile < total; tile += nwg) {
+    const int g = find_group(t0s, G, tile);
+    const GroupDesc gd = p.groups[g];
+    const WeightDesc wd = p.wtab[g];
+    const int local = tile - t0s[g];
+    const int nti = local / gd.mt;
+    const int m0 = (local - nti * gd.mt) * kBM;
+    const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
+
+    // Sources (rows clamped into the matrix so every load is in bounds;
+    // clamped rows and columns are never stored).  Wave w loads tile rows
+    // [w * 64, w * 64 + 64) of both operands; for gate/up that range is all
+    // gate or all up (tile rows [128 v, 128 v + 64) gate, the next 64 up).
+    const uint16_t* abase = A + (int64_t)(arow0 + m0) * K;
+    const int alast = gd.n - 1 - m0;
+    const uint16_t* bbase;
+    if (GATED)
+      bbase = reinterpret_cast<const uint16_t*>((wave & 1) ? wd.up : wd.gate);
+    else
+      bbase = reinterpret_cast<const uint16_t*>(wd.down);
+    uint32_t aoff[kNI], boff[kNI];
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) {
+      const int r = (wave * kNI + i) * kRPI + ld_row;  // tile row 0..255
+      aoff[i] = (uint32_t)(min(r, alast) * K + ld_c * 8);
+      int c = GATED ? nti * (kBN / 2) + (wave >> 1) * 64 + (r & 63) : nti * kBN + r;
+      c = min(c, n_out - 1);
+      boff[i] = (uint32_t)(c * K + ld_c * 8);
+    }
+
+#define DL_LOAD(kt_, st_)                                                                        \
+  do {                                                                                           \
+    const uint32_t sb_ = lds_base + (st_) * kStageB + wave * kNI * 1024;                          \
+    _Pragma("unroll") for (int i = 0; i < kNI; ++i)                                              \
+        dload16(abase + aoff[i] + (kt_) * BKS, sb_ + i * 1024);                                  \
+    _Pragma("unroll") for (int i = 0; i < kNI; ++i)                                              \
+        dload16(bbase + boff[i] + (kt_) * BKS, sb_ + kTileB + i * 1024);                         \
+  } while (0)
+#define DL_READ(st_, ks_, A_, B_)                                                                \
+  do {                                                                                           \
+    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
+    const int ro_ = rd_row * kRowB + (((2 * (ks_) + (lane >> 5)) ^ rd_s) << 4);                  \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) A_[i] =                                        \
+        *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * 128 + i * 32) * kRowB + ro_);             \
+    _Pragma("unroll") for (int j = 0; j < 4; ++j) B_[j] =                                        \
+        *reinterpret_cast<const bf16x8_t*>(ab_ + kTileB + (wn * 128 + j * 32) * kRowB + ro_);    \
+  } while (0)
+#define DL_MMA(A_, B_)                                                                           \
+  do {                                                                                           \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) _Pragma("unroll") for (int j = 0; j < 4; ++j)  \
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i], B_[j], acc[i][j], 0, 0, 0);   \
+  } while (0)
+#define DL_GROUP(st_, ks_, An, Bn, Ac, Bc)                                                       \
+  do {                                                                                           \
+    DL_READ(st_, ks_, An, Bn);                                                                   \
+    DL_MMA(Ac, Bc);                                                                              \
+    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                         \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+  } while (0)
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    // Nothing of this wave may still be in flight when the ring is refilled
+    // (the wait counter is in issue order, so earlier stores of the previous
+    // tile's epilogue would otherwise blur the counts below).
+    wait_vmcnt<0>();
+    __syncthreads();  // every wave is done with the previous tile's LDS
+#pragma unroll
+    for (int s = 0; s < kDist; ++s) DL_LOAD(min(s, KT - 1), s);
+    wait_vmcnt<(kDist - 1) * 2 * kNI>();  // step 0 has landed (this wave's part)
+    __syncthreads();                     // ... and every wave's part
+    DL_READ(0, 0, a0, b0);
+    // Step kt computes stage kt % STAGES and refills the stage read in step
+    // kt - 1 (every wave passed that step's barrier) with step kt + kDist.
+    // Past the last step the loads repeat the last step (never read).
+    int st = 0;
+    for (int kt = 0; kt < KT; ++kt) {
+      const int nst = st + 1 == STAGES ? 0 : st + 1;
+      const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
+      DL_LOAD(min(kt + kDist, KT - 1), fst);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (kSlices == 4) {
+        DL_GROUP(st, 1, a1, b1, a0, b0);
+        DL_GROUP(st, 2, a0, b0, a1, b1);
+        DL_GROUP(st, 3, a1, b1, a0, b0);
+      } else {
+        DL_GROUP(st, 1, a1, b1, a0, b0);
+      }
+      wait_vmcnt<(kDist - 1) * 2 * kNI>();  // step kt + 1 has landed
+      __syncthreads();
+      DL_GROUP(nst, 0, a0, b0, a1, b1);
+      st = nst;
+    }
+#undef DL_GROUP
+#undef DL_MMA
+#undef DL_READ
+#undef DL_LOAD
+
+    // Epilogue (as in ffn_mfma_kernel): stage bf16 results in LDS, write
+    // 16-byte chunks of whole rows.  The loads issued past the last step
+    // target the ring this staging reuses: let them land first.
+    wait_vmcnt<0>();
+    uint16_t* Cs = reinterpret_cast<uint16_t*>(smem);
+    constexpr int kPasses = GATED ? 1 : 2;
+#pragma unroll
+    for (int pass = 0; pass < kPasses; ++pass) {
+      __syncthreads();  // LDS reads of the K loop / previous pass are done
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = GATED ? jj : 2 * pass + jj;
+        const int cl = wn * 64 + jj * 32 + (lane & 31);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int rl = wm * 128 + i * 32 + c_row(lane, r);
+            float v;
+            if constexpr (GATED) {
+              const float gv = acc[i][j][r];
+              v = __fdividef(gv, 1.f + __expf(-gv)) * acc[i][j + 2][r];
+            } else {
+              v = acc[i][j][r];
+            }
+            Cs[rl * kEpiLd + cl] = (uint16_t)f32_to_bf16_rne(v);
+          }
+        }
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int it = 0; it < 16; ++it) {
+        const int q = tid + 256 * it;
+        const int rl = q >> 4, c16 = q & 15;
+        const int row = m0 + rl;
+        const int col = GATED ? nti * (kBN / 2) + c16 * 8 : nti * kBN + (c16 >> 3) * 128 + pass * 64 + (c16 & 7) * 8;
         if (row < gd.n && col < n_out) {
           const uint4 v = *reinterpret_cast<const uint4*>(&Cs[rl * kEpiLd + c16 * 8]);
           *reinterpret_cast<uint4*>(O + (int64_t)(gd.y_row0 + row) * n_out + col) = v;
@@ -412,9 +707,9 @@ hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* gr
       ffn_mfma_kernel<false, true><<<grid, 256, 0, s>>>(p);
   } else {
     if (stage == 0)
-      ffn_mfma_kernel<true, false><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<true, AEP_DL_BK, AEP_DL_STAGES><<<grid, 256, 0, s>>>(p);
     else
-      ffn_mfma_kernel<false, false><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<false, AEP_DL_BK, AEP_DL_STAGES><<<grid, 256, 0, s>>>(p);
   }
   return hipGetLastError();
 }
