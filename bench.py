@@ -44,6 +44,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1),
                     help="host threads for input generation")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-expert (weight-streaming) measurements")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also sweep rows per expert (16..256) on same-shape expert groups of >= 1 GB")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES three times (reference "
                          "kernel for scaling HBM byte counters) and exit")
@@ -190,11 +194,134 @@ def main():
         "setup_s": round(t_gen, 1),
     }
 
+    del ctx, wdev, xs, lgs, y, out
+    torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- cold experts
+    if not args.no_cold:
+        res["cold"] = cold_measurements(args)
+
     # ---------------------------------------------------------------- CPU oracle
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
 
     print(json.dumps(res), flush=True)
+
+
+def _flush(buf):
+    buf.add_(1)  # 1 GiB read + write: evicts L2 and the 256 MB Infinity Cache
+
+
+def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0):
+    """Grouped FFN over explicit per-expert rows (counts `groups`), weights of
+    the given format drawn on the device; returns (seconds per gate/up + down,
+    algorithmic bytes, flops).  Caches are flushed before every repetition."""
+    import torch
+    import paper_2505_08944_amd as aep
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    E = len(groups)
+    N = int(sum(groups))
+    ctx = aep.Context(1, E, d, f, 1, wdt=wdt, max_tokens_per_layer=max(N, 1))
+    W = []
+    for e in range(E):
+        if wdt == "fp8":
+            mats = [torch.randint(0, 126, s, generator=g, device=dev, dtype=torch.uint8)
+                    for s in [(f, d), (f, d), (d, f)]]
+            sc = [torch.full((2 * f,), 1.0, dtype=torch.bfloat16, device=dev) * 0.001,
+                  torch.full((d,), 1.0, dtype=torch.bfloat16, device=dev) * 0.001]
+        else:
+            mats = [(torch.randn(s, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+                    for s in [(f, d), (f, d), (d, f)]]
+            sc = [None, None]
+        ctx.set_expert_weights(0, e, *mats, *sc)
+        W.append(mats + sc)
+    rows = [torch.randn((n, d), generator=g, device=dev).to(torch.bfloat16) for n in groups]
+    tok = torch.arange(N, dtype=torch.int32, device=dev)
+    gw = torch.ones(N, dtype=torch.float32, device=dev)
+    o = 0
+    for e, n in enumerate(groups):
+        if n:
+            ctx.enqueue_rows(0, e, rows[e], tok[o:o + n], gw[o:o + n], N)
+        o += n
+    b = ctx.rebatch(0)
+    y = torch.empty((b.n_rows, d), dtype=torch.bfloat16, device=dev)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    ctx.expert_gate_up(b)
+    ctx.expert_down(b, y)
+    times = []
+    for _ in range(reps):
+        _flush(flush)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ctx.expert_gate_up(b)
+        ctx.expert_down(b, y)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / 1e3)
+    ctx.release(b)
+    ctx.sync()
+    wbytes = 3 * d * f * (1 if wdt == "fp8" else 2) + (2 * (2 * f + d) if wdt == "fp8" else 0)
+    nonempty = sum(1 for n in groups if n)
+    byts = nonempty * wbytes + N * 2 * d * 2
+    t = float(np.median(times))
+    del ctx, W, rows, flush
+    torch.cuda.empty_cache()
+    return t, byts, 6.0 * d * f * N
+
+
+def cold_measurements(args):
+    """Weight-streaming side of the metric: experts with <= 256 queued rows.
+
+    * fine-grained layer (d=2048, ffn=1408): the cold experts of the routed
+      64-expert layer (their counts from the same synthetic routing);
+    * one GPU's EP share (d=4096, ffn=2048): the cold experts of the Zipf
+      depths, bf16 and fp8 weights;
+    * with --sweep: G same-shape experts x n rows, G chosen for >= 1 GB of weights.
+    """
+    import synth
+    import torch
+    import paper_2505_08944_amd as aep
+    out = {}
+    # fine-grained layer: routed counts
+    w3 = synth.workload("c3")
+    frags = synth.layer_fragments(w3, 0)
+    T = sum(f["x"].shape[0] for f in frags)
+    ctx = aep.Context(1, w3.E, w3.d, w3.f, w3.k, n_shared=w3.S, max_tokens_per_layer=T)
+    for f in frags:
+        x = torch.from_numpy(f["x"].view(np.int16)).view(torch.bfloat16).cuda()
+        lg = torch.from_numpy(f["logits"]).cuda()
+        ctx.route_enqueue(0, x, lg)
+    counts3 = ctx.expert_counts(0).tolist()
+    del ctx
+    cold3 = [n for n in counts3 if 0 < n <= 256]
+    t, byts, fl = time_rows_ffn(cold3, w3.d, w3.f, "bf16")
+    out["finegrained_d2048_f1408_bf16"] = {"experts": len(cold3), "rows": sum(cold3), "ms": round(t * 1e3, 4),
+                                           "GBps": round(byts / t / 1e9, 1),
+                                           "hbm_frac": round(byts / t / 1e9 / PEAK_HBM_GBS, 4),
+                                           "bytes": byts}
+    w4 = synth.workload("c4")
+    depths = synth.rows_workload(w4)["depths"].tolist()
+    cold4 = [n for n in depths if n <= 256]
+    for wdt in ("bf16", "fp8"):
+        t, byts, fl = time_rows_ffn(cold4, w4.d, w4.f, wdt)
+        out[f"ep_share_d4096_f2048_{wdt}"] = {"experts": len(cold4), "rows": sum(cold4), "ms": round(t * 1e3, 4),
+                                             "GBps": round(byts / t / 1e9, 1),
+                                             "hbm_frac": round(byts / t / 1e9 / PEAK_HBM_GBS, 4), "bytes": byts}
+    if args.sweep:
+        sweep = {}
+        for (d, f) in [(2048, 1408), (4096, 2048), (4096, 14336)]:
+            for wdt in ("bf16", "fp8"):
+                per = 3 * d * f * (1 if wdt == "fp8" else 2)
+                G = max(1, -(-(1 << 30) // per))
+                for n in (16, 32, 64, 128, 256):
+                    t, byts, fl = time_rows_ffn([n] * G, d, f, wdt)
+                    sweep[f"d{d}_f{f}_{wdt}_n{n}"] = {"G": G, "ms": round(t * 1e3, 4),
+                                                      "hbm_frac": round(byts / t / 1e9 / PEAK_HBM_GBS, 4),
+                                                      "tflops": round(fl / t / 1e12, 1)}
+        out["sweep"] = sweep
+    return out
 
 
 def cpu_baseline(w, n_tok: int):

@@ -31,18 +31,21 @@ struct WeightDesc {
 };
 static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 
-// One FFN group of a drained batch, written by the plan kernel.
+// One FFN group of a drained batch, written by the plan kernel.  A group's
+// rows are covered by up to two row-tile families: "big" tiles (256 rows for
+// bf16/fp8 weights, 64 for f32) over rows [0, nbig * big_bm), clamped to n,
+// and "small" 64-row tiles over rows [small_row0, n).
 struct GroupDesc {
-  int32_t n;       // rows
-  int32_t x_row0;  // first row in x_perm
-  int32_t y_row0;  // first row in h and y
-  int32_t bm;      // row-tile height used for this group
-  int32_t tile0_gu;  // first gate/up tile of the group
-  int32_t tile0_dn;  // first down tile of the group
-  int32_t mt;        // row tiles
-  int32_t pad;
+  int32_t n;           // rows
+  int32_t x_row0;      // first row in x_perm
+  int32_t y_row0;      // first row in h and y
+  int32_t nbig;        // big row tiles
+  int32_t nsmall;      // small row tiles
+  int32_t small_row0;  // first row of the small tiles
+  int32_t t0[4];       // first tile: gate/up big, gate/up small, down big, down small
+  int32_t pad[2];
 };
-static_assert(sizeof(GroupDesc) == 32, "GroupDesc layout");
+static_assert(sizeof(GroupDesc) == 48, "GroupDesc layout");
 
 // Device error flag bits.
 constexpr int32_t kErrNonFinite = 1;
@@ -60,6 +63,8 @@ constexpr int kMaxGroups = 1024;
 constexpr int kBM = 256;
 constexpr int kBN = 256;
 constexpr int kBK = 64;
+constexpr int kSmallBM = 64;   // small-family tiles (bf16 weights): 64 rows ...
+constexpr int kSmallBN = 128;  // ... x 128 columns (gate/up: 64 features)
 // f32 path
 constexpr int kBM32 = 64;
 constexpr int kBN32 = 64;
@@ -79,9 +84,12 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
                                int k, int expert, int E, const int32_t* depth_cur,
                                int32_t* depth_nxt, QEntry* q, int64_t q_stride, int32_t* err,
                                hipStream_t s);
+// tile_totals[4]: gate/up big, gate/up small, down big, down small.  nt[4]:
+// column tiles per row tile in the same order.  small_bm = 0 disables the
+// small family (every row in big tiles of big_bm).
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int32_t* depth, int32_t* counts,
-                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, int nt_gu,
-                       int nt_dn, int bm, int32_t* pos, float* posw, hipStream_t s);
+                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, const int* nt,
+                       int big_bm, int small_bm, int32_t* pos, float* posw, hipStream_t s);
 hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,
                          int64_t N, int n_tokens, int shared, const void* const* tok_row,
                          char* xp, int64_t row_bytes, int32_t* row_token, float* row_w,

@@ -94,7 +94,7 @@ bool layout(Ctx& c) {
   c.off_counts = take(sizeof(int32_t) * c.G);
   c.off_offsets = take(sizeof(int32_t) * (c.G + 1));
   c.off_groups = take(sizeof(GroupDesc) * c.G);
-  c.off_tiles = take(sizeof(int32_t) * 2);
+  c.off_tiles = take(sizeof(int32_t) * 4);
   c.off_xp = take((size_t)xrows * d * c.esz);
   c.off_rowtok = take(sizeof(int32_t) * N);
   c.off_roww = take(sizeof(float) * N);
@@ -111,17 +111,25 @@ hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE; }
 
-// column tiles and row-tile height of the FFN launches
-void tiling(const Ctx& c, int* nt_gu, int* nt_dn, int* bm) {
+// Tiling of the FFN launches: nt[4] = column tiles per row tile (gate/up big,
+// gate/up small, down big, down small) and the row-tile heights.  f32 uses
+// 64 x 64 tiles only; bf16 weights use 256 x 256 tiles plus the 64 x 128
+// small family; fp8 weights use 256 x 256 tiles only.
+void tiling(const Ctx& c, int nt[4], int* big_bm, int* small_bm) {
   const int d = c.cfg.d_model, f = c.cfg.d_ffn;
+  auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
   if (c.cfg.act_dtype == AEP_F32) {
-    *nt_gu = (f + kBN32 - 1) / kBN32;
-    *nt_dn = (d + kBN32 - 1) / kBN32;
-    *bm = kBM32;
+    nt[0] = nt[1] = cdiv(f, kBN32);
+    nt[2] = nt[3] = cdiv(d, kBN32);
+    *big_bm = kBM32;
+    *small_bm = 0;
   } else {
-    *nt_gu = (f + kBN / 2 - 1) / (kBN / 2);
-    *nt_dn = (d + kBN - 1) / kBN;
-    *bm = kBM;
+    nt[0] = cdiv(f, kBN / 2);
+    nt[1] = cdiv(f, kSmallBN / 2);
+    nt[2] = cdiv(d, kBN);
+    nt[3] = cdiv(d, kSmallBN);
+    *big_bm = kBM;
+    *small_bm = c.cfg.w_dtype == AEP_BF16 ? kSmallBM : 0;
   }
 }
 
@@ -381,8 +389,8 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   if (L.rows == 0 && !(c->cfg.n_shared > 0 && L.tokens > 0)) return AEP_ERR_EMPTY;
   for (int g = 0; g < c->G; ++g)
     if (!L.have_w[g]) return AEP_ERR_STATE;
-  int nt_gu, nt_dn, bm;
-  tiling(*c, &nt_gu, &nt_dn, &bm);
+  int nt[4], big_bm, small_bm;
+  tiling(*c, nt, &big_bm, &small_bm);
   hipStream_t s = as_stream(stream);
   const int E = c->cfg.n_experts, S = c->cfg.n_shared, k = c->cfg.top_k;
   int32_t* counts = c->at<int32_t>(c->off_counts);
@@ -390,7 +398,7 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   int32_t* pos = c->at<int32_t>(c->off_pos);
   float* posw = c->at<float>(c->off_posw);
   if (launch_plan(E, S, L.tokens, k, c->depth(layer, L.cur), counts, offsets, c->at<GroupDesc>(c->off_groups),
-                  c->at<int32_t>(c->off_tiles), nt_gu, nt_dn, bm, pos, posw, s) != hipSuccess)
+                  c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, pos, posw, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, L.rows, L.tokens, S > 0, c->tokrow(layer),
@@ -429,12 +437,14 @@ static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, 
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
   if (stage == 1 && !y) return AEP_ERR_INVALID_ARG;
-  int nt_gu, nt_dn, bm;
-  tiling(*c, &nt_gu, &nt_dn, &bm);
-  const int64_t E = c->cfg.n_experts, S = c->cfg.n_shared;
+  int nt[4], big_bm, small_bm;
+  tiling(*c, nt, &big_bm, &small_bm);
+  const int64_t E = c->cfg.n_experts, S = c->cfg.n_shared, G = E + S;
   const int64_t N = batch->n_routed, T = batch->n_tokens;
-  const int64_t row_tiles = N / bm + std::min<int64_t>(E, N) + S * ((T + bm - 1) / bm);
-  const int64_t mt = row_tiles * (stage == 0 ? nt_gu : nt_dn);
+  // bound on tiles: every group's rows in big tiles, plus at most 3 small row
+  // tiles per group
+  const int64_t big_rows = N / big_bm + std::min<int64_t>(E, N) + S * ((T + big_bm - 1) / big_bm);
+  const int64_t mt = big_rows * nt[stage == 0 ? 0 : 2] + (small_bm ? 3 * G * nt[stage == 0 ? 1 : 3] : 0);
   if (mt > INT32_MAX) return AEP_ERR_UNSUPPORTED;
   return dev(launch_ffn(stage, c->cfg.act_dtype, c->cfg.w_dtype, c->at<GroupDesc>(c->off_groups),
                         c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles), (int)mt,

@@ -103,8 +103,8 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int G = p.G;
-  const int total = p.tile_totals[GATED ? 0 : 1];
-  for (int g = tid; g < G; g += 256) t0s[g] = GATED ? p.groups[g].tile0_gu : p.groups[g].tile0_dn;
+  const int total = p.tile_totals[GATED ? 0 : 2];
+  for (int g = tid; g < G; g += 256) t0s[g] = p.groups[g].t0[GATED ? 0 : 2];
   if (tid == 0) t0s[G] = total;
   __syncthreads();
 
@@ -119,8 +119,8 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
     const GroupDesc gd = p.groups[g];
     const WeightDesc wd = p.wtab[g];
     const int local = tile - t0s[g];
-    const int nti = local / gd.mt;
-    const int m0 = (local - nti * gd.mt) * kBM;
+    const int nti = local / gd.nbig;
+    const int m0 = (local - nti * gd.nbig) * kBM;
     const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
 
     // Global sources of this thread's 16-byte chunks: a uniform 64-bit base
@@ -368,12 +368,6 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
 // over distinct banks (s(r) = r % 8 for 128-byte rows, (r / 2) % 4 for
 // 64-byte rows).  Each lane picks the global chunk that belongs at its fixed
 // LDS position, so the swizzle costs nothing at load time.
-#ifndef AEP_DL_BK
-#define AEP_DL_BK 64
-#endif
-#ifndef AEP_DL_STAGES
-#define AEP_DL_STAGES 2
-#endif
 typedef __attribute__((address_space(3))) void* lds_vptr;
 typedef const __attribute__((address_space(1))) void* glb_vptr;
 
@@ -395,193 +389,235 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
 }
 
-template <bool GATED, int BKS, int STAGES>
-__global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
-  constexpr int kRowB = BKS * 2;         // bytes of one tile row per K step
-  constexpr int kCPR = BKS / 8;          // 16-byte chunks per row
-  constexpr int kRPI = 1024 / kRowB;     // rows per direct-load instruction
-  constexpr int kNI = kBM / kRPI / 4;    // direct loads per wave per operand per K step
-  constexpr int kTileB = kBM * kRowB;    // bytes of one operand tile per K step
-  constexpr int kStageB = 2 * kTileB;
-  constexpr int kSlices = BKS / 16;
+// One output tile of BM rows x BN columns (gate/up: BN/2 features of gate and
+// the same BN/2 of up) at row m0 of group gd, column tile nti.  Four waves in
+// a 2 x 2 grid, each owning a (BM/2) x (BN/2) block of 32 x 32 MFMA
+// fragments.  STAGES LDS buffers of (BM + BN) x 128 bytes form the ring
+// (prefetch distance STAGES - 1 K steps of 64).
+template <bool GATED, int BM, int BN, int STAGES>
+__device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem, uint32_t lds_base,
+                                        const GroupDesc& gd, const WeightDesc& wd, int nti, int m0) {
+  constexpr int BKS = kBK;
+  constexpr int kRowB = BKS * 2;              // 128 bytes: one tile row of one K step
+  constexpr int TM = BM / 2, TN = BN / 2;     // wave tile
+  constexpr int MI = TM / 32, NI = TN / 32;   // 32 x 32 fragments per wave
+  constexpr int kNA = BM / 8 / 4;             // direct loads per wave per K step: A (8 rows each)
+  constexpr int kNB = BN / 8 / 4;             // ... and B
+  constexpr int kTileA = BM * kRowB, kStageB = (BM + BN) * kRowB;
   constexpr int kDist = STAGES - 1;
-  static_assert(kBM == kBN, "square tiles");
-  static_assert(STAGES * kStageB >= kBM * kEpiLd * 2, "epilogue staging must fit");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * kStageB];
-  __shared__ int32_t t0s[kMaxGroups + 1];
+  constexpr int kPerStep = kNA + kNB;
+  constexpr int kLd = BN / 2 + 8;             // epilogue staging row stride (bf16)
+  static_assert(MI >= 1 && NI >= 2 && NI % 2 == 0, "wave tile");
+  static_assert(STAGES * kStageB <= 2 * (kBM + kBN) * kRowB, "ring must fit the shared buffer");
+  static_assert(BM * kLd * 2 <= 2 * (kBM + kBN) * kRowB, "epilogue staging must fit");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int G = p.G;
-  const int total = p.tile_totals[GATED ? 0 : 1];
-  for (int g = tid; g < G; g += 256) t0s[g] = GATED ? p.groups[g].tile0_gu : p.groups[g].tile0_dn;
-  if (tid == 0) t0s[G] = total;
-  __syncthreads();
-
-  const int nwg = gridDim.x;
-  const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
   const int K = p.K, KT = K / BKS, n_out = p.n_out;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
   uint16_t* O = reinterpret_cast<uint16_t*>(p.out);
-
-  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
-  // loader lane constants: row within an instruction's block, LDS position,
-  // and the k chunk that belongs there
-  const int ld_row = lane / kCPR;
-  const int ld_c = (lane % kCPR) ^ (kCPR == 8 ? (lane >> 3) : ((lane >> 3) & 3));
-  // reader lane constants: fragment row and its swizzle
+  // loader: lane l fills LDS position l % 8 of row l / 8 of an 8-row block with
+  // the k chunk that belongs there, (l % 8) ^ (row % 8)
+  const int ld_row = lane >> 3;
+  const int ld_c = (lane & 7) ^ (lane >> 3);
+  // reader: fragment row and its swizzle
   const int rd_row = lane & 31;
-  const int rd_s = kCPR == 8 ? (rd_row & 7) : ((rd_row >> 1) & 3);
+  const int rd_s = rd_row & 7;
 
-  for (int tile = slot; tile < total; tile += nwg) {
-    const int g = find_group(t0s, G, tile);
-    const GroupDesc gd = p.groups[g];
-    const WeightDesc wd = p.wtab[g];
-    const int local = tile - t0s[g];
-    const int nti = local / gd.mt;
-    const int m0 = (local - nti * gd.mt) * kBM;
-    const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
-
-    // Sources (rows clamped into the matrix so every load is in bounds;
-    // clamped rows and columns are never stored).  Wave w loads tile rows
-    // [w * 64, w * 64 + 64) of both operands; for gate/up that range is all
-    // gate or all up (tile rows [128 v, 128 v + 64) gate, the next 64 up).
-    const uint16_t* abase = A + (int64_t)(arow0 + m0) * K;
-    const int alast = gd.n - 1 - m0;
-    const uint16_t* bbase;
-    if (GATED)
-      bbase = reinterpret_cast<const uint16_t*>((wave & 1) ? wd.up : wd.gate);
-    else
-      bbase = reinterpret_cast<const uint16_t*>(wd.down);
-    uint32_t aoff[kNI], boff[kNI];
+  const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
+  const uint16_t* abase = A + (int64_t)(arow0 + m0) * K;
+  const int alast = gd.n - 1 - m0;
+  uint32_t aoff[kNA], boff[kNB];
 #pragma unroll
-    for (int i = 0; i < kNI; ++i) {
-      const int r = (wave * kNI + i) * kRPI + ld_row;  // tile row 0..255
-      aoff[i] = (uint32_t)(min(r, alast) * K + ld_c * 8);
-      int c = GATED ? nti * (kBN / 2) + (wave >> 1) * 64 + (r & 63) : nti * kBN + r;
-      c = min(c, n_out - 1);
-      boff[i] = (uint32_t)(c * K + ld_c * 8);
+  for (int i = 0; i < kNA; ++i) aoff[i] = (uint32_t)(min((wave * kNA + i) * 8 + ld_row, alast) * K + ld_c * 8);
+  // B rows: a wave column's TN rows are TN/2 gate features then the same TN/2
+  // up features; an 8-row load block never straddles the two halves.
+  const uint16_t* bsrc[kNB];
+#pragma unroll
+  for (int i = 0; i < kNB; ++i) {
+    const int br = (wave * kNB + i) * 8 + ld_row;
+    int c;
+    bool up = false;
+    if (GATED) {
+      const int within = br % TN;
+      up = within >= TN / 2;
+      c = nti * (BN / 2) + (br / TN) * (TN / 2) + within % (TN / 2);
+    } else {
+      c = nti * BN + br;
     }
+    c = min(c, n_out - 1);
+    boff[i] = (uint32_t)(c * K + ld_c * 8);
+    bsrc[i] = reinterpret_cast<const uint16_t*>(GATED ? (up ? wd.up : wd.gate) : wd.down);
+  }
 
 #define DL_LOAD(kt_, st_)                                                                        \
   do {                                                                                           \
-    const uint32_t sb_ = lds_base + (st_) * kStageB + wave * kNI * 1024;                          \
-    _Pragma("unroll") for (int i = 0; i < kNI; ++i)                                              \
-        dload16(abase + aoff[i] + (kt_) * BKS, sb_ + i * 1024);                                  \
-    _Pragma("unroll") for (int i = 0; i < kNI; ++i)                                              \
-        dload16(bbase + boff[i] + (kt_) * BKS, sb_ + kTileB + i * 1024);                         \
+    const uint32_t sa_ = lds_base + (st_) * kStageB + wave * kNA * 1024;                          \
+    const uint32_t sb_ = lds_base + (st_) * kStageB + kTileA + wave * kNB * 1024;                 \
+    _Pragma("unroll") for (int i = 0; i < kNA; ++i)                                              \
+        dload16(abase + aoff[i] + (kt_) * BKS, sa_ + i * 1024);                                  \
+    _Pragma("unroll") for (int i = 0; i < kNB; ++i)                                              \
+        dload16(bsrc[i] + boff[i] + (kt_) * BKS, sb_ + i * 1024);                                \
   } while (0)
 #define DL_READ(st_, ks_, A_, B_)                                                                \
   do {                                                                                           \
     const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
     const int ro_ = rd_row * kRowB + (((2 * (ks_) + (lane >> 5)) ^ rd_s) << 4);                  \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) A_[i] =                                        \
-        *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * 128 + i * 32) * kRowB + ro_);             \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j) B_[j] =                                        \
-        *reinterpret_cast<const bf16x8_t*>(ab_ + kTileB + (wn * 128 + j * 32) * kRowB + ro_);    \
+    _Pragma("unroll") for (int i = 0; i < MI; ++i) A_[i] =                                       \
+        *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + i * 32) * kRowB + ro_);              \
+    _Pragma("unroll") for (int j = 0; j < NI; ++j) B_[j] =                                       \
+        *reinterpret_cast<const bf16x8_t*>(ab_ + kTileA + (wn * TN + j * 32) * kRowB + ro_);     \
   } while (0)
 #define DL_MMA(A_, B_)                                                                           \
   do {                                                                                           \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) _Pragma("unroll") for (int j = 0; j < 4; ++j)  \
+    _Pragma("unroll") for (int i = 0; i < MI; ++i) _Pragma("unroll") for (int j = 0; j < NI; ++j) \
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i], B_[j], acc[i][j], 0, 0, 0);   \
   } while (0)
+  // operand reads spread between the MFMAs
+  constexpr int kQ = MI * NI >= 4 ? 4 : MI * NI;
 #define DL_GROUP(st_, ks_, An, Bn, Ac, Bc)                                                       \
   do {                                                                                           \
     DL_READ(st_, ks_, An, Bn);                                                                   \
     DL_MMA(Ac, Bc);                                                                              \
-    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                         \
+    _Pragma("unroll") for (int q_ = 0; q_ < kQ; ++q_) {                                          \
+      __builtin_amdgcn_sched_group_barrier(0x100, (MI + NI + kQ - 1) / kQ, 0);                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, MI * NI / kQ, 0);                              \
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
   } while (0)
 
-    f32x16_t acc[4][4];
+  f32x16_t acc[MI][NI];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NI; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    bf16x8_t a0[4], b0[4], a1[4], b1[4];
-    // Nothing of this wave may still be in flight when the ring is refilled
-    // (the wait counter is in issue order, so earlier stores of the previous
-    // tile's epilogue would otherwise blur the counts below).
-    wait_vmcnt<0>();
-    __syncthreads();  // every wave is done with the previous tile's LDS
+  bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
+  // Nothing of this wave may still be in flight when the ring is refilled
+  // (the wait counter is in issue order, so earlier stores of the previous
+  // tile's epilogue would otherwise blur the counts below).
+  wait_vmcnt<0>();
+  __syncthreads();  // every wave is done with the previous tile's LDS
 #pragma unroll
-    for (int s = 0; s < kDist; ++s) DL_LOAD(min(s, KT - 1), s);
-    wait_vmcnt<(kDist - 1) * 2 * kNI>();  // step 0 has landed (this wave's part)
-    __syncthreads();                     // ... and every wave's part
-    DL_READ(0, 0, a0, b0);
-    // Step kt computes stage kt % STAGES and refills the stage read in step
-    // kt - 1 (every wave passed that step's barrier) with step kt + kDist.
-    // Past the last step the loads repeat the last step (never read).
-    int st = 0;
-    for (int kt = 0; kt < KT; ++kt) {
-      const int nst = st + 1 == STAGES ? 0 : st + 1;
-      const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
-      DL_LOAD(min(kt + kDist, KT - 1), fst);
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (kSlices == 4) {
-        DL_GROUP(st, 1, a1, b1, a0, b0);
-        DL_GROUP(st, 2, a0, b0, a1, b1);
-        DL_GROUP(st, 3, a1, b1, a0, b0);
-      } else {
-        DL_GROUP(st, 1, a1, b1, a0, b0);
-      }
-      wait_vmcnt<(kDist - 1) * 2 * kNI>();  // step kt + 1 has landed
-      __syncthreads();
-      DL_GROUP(nst, 0, a0, b0, a1, b1);
-      st = nst;
-    }
+  for (int s = 0; s < kDist; ++s) DL_LOAD(min(s, KT - 1), s);
+  wait_vmcnt<(kDist - 1) * kPerStep>();  // step 0 has landed (this wave's part)
+  __syncthreads();                       // ... and every wave's part
+  DL_READ(0, 0, a0, b0);
+  // Step kt computes stage kt % STAGES and refills the stage read in step
+  // kt - 1 (every wave passed that step's barrier) with step kt + kDist.
+  // Past the last step the loads repeat the last step (never read).
+  int st = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int nst = st + 1 == STAGES ? 0 : st + 1;
+    const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
+    DL_LOAD(min(kt + kDist, KT - 1), fst);
+    __builtin_amdgcn_sched_barrier(0);
+    DL_GROUP(st, 1, a1, b1, a0, b0);
+    DL_GROUP(st, 2, a0, b0, a1, b1);
+    DL_GROUP(st, 3, a1, b1, a0, b0);
+    wait_vmcnt<(kDist - 1) * kPerStep>();  // step kt + 1 has landed
+    __syncthreads();
+    DL_GROUP(nst, 0, a0, b0, a1, b1);
+    st = nst;
+  }
 #undef DL_GROUP
 #undef DL_MMA
 #undef DL_READ
 #undef DL_LOAD
 
-    // Epilogue (as in ffn_mfma_kernel): stage bf16 results in LDS, write
-    // 16-byte chunks of whole rows.  The loads issued past the last step
-    // target the ring this staging reuses: let them land first.
-    wait_vmcnt<0>();
-    uint16_t* Cs = reinterpret_cast<uint16_t*>(smem);
-    constexpr int kPasses = GATED ? 1 : 2;
+  // Epilogue: stage bf16 results in LDS ([BM][BN/2 + 8]) and write 16-byte
+  // chunks of whole rows.  Gate/up: one pass, feature fragment j pairs with
+  // up fragment j + NI/2.  Down: two passes of BN/2 columns (each wave
+  // contributes column fragments pass * NI/2 .. pass * NI/2 + NI/2 - 1).
+  // The loads issued past the last step target the ring this reuses: let
+  // them land first.
+  wait_vmcnt<0>();
+  uint16_t* Cs = reinterpret_cast<uint16_t*>(smem);
+  constexpr int kPasses = GATED ? 1 : 2;
+  constexpr int kChunks = BN / 16;  // 16-byte chunks per staged row
 #pragma unroll
-    for (int pass = 0; pass < kPasses; ++pass) {
-      __syncthreads();  // LDS reads of the K loop / previous pass are done
+  for (int pass = 0; pass < kPasses; ++pass) {
+    __syncthreads();  // LDS reads of the K loop / previous pass are done
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int j = GATED ? jj : 2 * pass + jj;
-        const int cl = wn * 64 + jj * 32 + (lane & 31);
+    for (int jj = 0; jj < NI / 2; ++jj) {
+      const int j = GATED ? jj : pass * (NI / 2) + jj;
+      const int cl = wn * (TN / 2) + jj * 32 + (lane & 31);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < MI; ++i) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int rl = wm * 128 + i * 32 + c_row(lane, r);
-            float v;
-            if constexpr (GATED) {
-              const float gv = acc[i][j][r];
-              v = __fdividef(gv, 1.f + __expf(-gv)) * acc[i][j + 2][r];
-            } else {
-              v = acc[i][j][r];
-            }
-            Cs[rl * kEpiLd + cl] = (uint16_t)f32_to_bf16_rne(v);
+        for (int r = 0; r < 16; ++r) {
+          const int rl = wm * TM + i * 32 + c_row(lane, r);
+          float v;
+          if constexpr (GATED) {
+            const float gv = acc[i][j][r];
+            v = __fdividef(gv, 1.f + __expf(-gv)) * acc[i][j + NI / 2][r];
+          } else {
+            v = acc[i][j][r];
           }
+          Cs[rl * kLd + cl] = (uint16_t)f32_to_bf16_rne(v);
         }
       }
-      __syncthreads();
+    }
+    __syncthreads();
 #pragma unroll 4
-      for (int it = 0; it < 16; ++it) {
-        const int q = tid + 256 * it;
-        const int rl = q >> 4, c16 = q & 15;
-        const int row = m0 + rl;
-        const int col = GATED ? nti * (kBN / 2) + c16 * 8 : nti * kBN + (c16 >> 3) * 128 + pass * 64 + (c16 & 7) * 8;
-        if (row < gd.n && col < n_out) {
-          const uint4 v = *reinterpret_cast<const uint4*>(&Cs[rl * kEpiLd + c16 * 8]);
-          *reinterpret_cast<uint4*>(O + (int64_t)(gd.y_row0 + row) * n_out + col) = v;
-        }
+    for (int it = 0; it < BM * kChunks / 256; ++it) {
+      const int q = tid + 256 * it;
+      const int rl = q / kChunks, cc = q % kChunks;
+      const int row = m0 + rl;
+      const int sc = cc * 8;  // staged column
+      const int col = GATED ? nti * (BN / 2) + sc
+                            : nti * BN + (sc / (TN / 2)) * TN + pass * (TN / 2) + sc % (TN / 2);
+      if (row < gd.n && col < n_out) {
+        const uint4 v = *reinterpret_cast<const uint4*>(&Cs[rl * kLd + sc]);
+        *reinterpret_cast<uint4*>(O + (int64_t)(gd.y_row0 + row) * n_out + col) = v;
       }
+    }
+  }
+}
+
+// bf16-weight FFN launch: every tile of the big family (256 rows), then every
+// tile of the small family (64 rows: cold experts and the ragged tails of hot
+// ones), in one persistent grid.  Small tiles come last, so they also fill
+// the tail of the big ones.  Small tiles are 64 rows x 128 columns: cold
+// experts are weight-streaming bound, and narrower tiles spread each expert's
+// weights over more CUs.
+template <bool GATED>
+__global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * (kBM + kBN) * kBK * 2];
+  __shared__ int32_t t0b[kMaxGroups + 1], t0s[kMaxGroups + 1];
+  const int tid = threadIdx.x;
+  const int G = p.G;
+  const int big_total = p.tile_totals[GATED ? 0 : 2];
+  const int small_total = p.tile_totals[GATED ? 1 : 3];
+  for (int g = tid; g < G; g += 256) {
+    t0b[g] = p.groups[g].t0[GATED ? 0 : 2];
+    t0s[g] = p.groups[g].t0[GATED ? 1 : 3];
+  }
+  if (tid == 0) {
+    t0b[G] = big_total;
+    t0s[G] = small_total;
+  }
+  __syncthreads();
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
+  const int nwg = gridDim.x;
+  const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
+  for (int tile = slot; tile < big_total + small_total; tile += nwg) {
+    if (tile < big_total) {
+      const int g = find_group(t0b, G, tile);
+      const GroupDesc gd = p.groups[g];
+      const int local = tile - t0b[g];
+      const int nti = local / gd.nbig;
+      dl_tile<GATED, kBM, kBN, 2>(p, smem, lds_base, gd, p.wtab[g], nti, (local - nti * gd.nbig) * kBM);
+    } else {
+      const int t = tile - big_total;
+      const int g = find_group(t0s, G, t);
+      const GroupDesc gd = p.groups[g];
+      const int local = t - t0s[g];
+      const int nti = local / gd.nsmall;
+      dl_tile<GATED, kSmallBM, kSmallBN, 4>(p, smem, lds_base, gd, p.wtab[g], nti,
+                                  gd.small_row0 + (local - nti * gd.nsmall) * kSmallBM);
     }
   }
 }
@@ -596,8 +632,8 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(const FfnParams p) {
   __shared__ int32_t t0s[kMaxGroups + 1];
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
   const int G = p.G;
-  const int total = p.tile_totals[GATED ? 0 : 1];
-  for (int g = tid; g < G; g += 256) t0s[g] = GATED ? p.groups[g].tile0_gu : p.groups[g].tile0_dn;
+  const int total = p.tile_totals[GATED ? 0 : 2];
+  for (int g = tid; g < G; g += 256) t0s[g] = p.groups[g].t0[GATED ? 0 : 2];
   if (tid == 0) t0s[G] = total;
   __syncthreads();
   const int K = p.K, n_out = p.n_out;
@@ -609,8 +645,8 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(const FfnParams p) {
     const GroupDesc gd = p.groups[g];
     const WeightDesc wd = p.wtab[g];
     const int local = tile - t0s[g];
-    const int nti = local / gd.mt;
-    const int m0 = (local - nti * gd.mt) * BM;
+    const int nti = local / gd.nbig;
+    const int m0 = (local - nti * gd.nbig) * BM;
     const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
     const int lr = tid >> 2, lk = (tid & 3) * 4;
     const float* asrc = A + (int64_t)(arow0 + min(m0 + lr, gd.n - 1)) * K + lk;
@@ -707,9 +743,9 @@ hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* gr
       ffn_mfma_kernel<false, true><<<grid, 256, 0, s>>>(p);
   } else {
     if (stage == 0)
-      ffn_dlds_kernel<true, AEP_DL_BK, AEP_DL_STAGES><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<true><<<grid, 256, 0, s>>>(p);
     else
-      ffn_dlds_kernel<false, AEP_DL_BK, AEP_DL_STAGES><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<false><<<grid, 256, 0, s>>>(p);
   }
   return hipGetLastError();
 }

@@ -20,8 +20,10 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
                                                     int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ offsets,
                                                     GroupDesc* __restrict__ groups,
-                                                    int32_t* __restrict__ tile_totals, int nt_gu,
-                                                    int nt_dn, int bm, int32_t* __restrict__ pos,
+                                                    int32_t* __restrict__ tile_totals, int nt0,
+                                                    int nt1, int nt2, int nt3, int big_bm,
+                                                    int small_bm,
+                                                    int32_t* __restrict__ pos,
                                                     float* __restrict__ posw) {
   __shared__ int32_t cnt[kMaxGroups];
   const int tid = threadIdx.x;
@@ -31,29 +33,46 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
   if (tid == 0) {
     int N = 0;
     for (int g = 0; g < E; ++g) N += cnt[g];
-    int off = 0, tg = 0, td = 0;
+    int off = 0;
+    int t[4] = {0, 0, 0, 0};
     for (int g = 0; g < G; ++g) {
       const int n = cnt[g];
-      const int mt = (n + bm - 1) / bm;
+      int nbig, nsmall = 0;
+      if (small_bm == 0) {
+        nbig = (n + big_bm - 1) / big_bm;
+      } else {
+        // Full big tiles, then the remainder in small tiles unless it would
+        // take more than 3 of them (then one more big tile is as cheap).
+        const int full = n / big_bm, r = n - full * big_bm;
+        nbig = full;
+        if (r > 3 * small_bm)
+          nbig += 1;
+        else
+          nsmall = (r + small_bm - 1) / small_bm;
+      }
       GroupDesc gd;
       gd.n = n;
       gd.x_row0 = g < E ? off : N;
       gd.y_row0 = off;
-      gd.bm = bm;
-      gd.tile0_gu = tg;
-      gd.tile0_dn = td;
-      gd.mt = mt;
-      gd.pad = 0;
+      gd.nbig = nbig;
+      gd.nsmall = nsmall;
+      gd.small_row0 = (n / big_bm) * big_bm;
+      gd.t0[0] = t[0];
+      gd.t0[1] = t[1];
+      gd.t0[2] = t[2];
+      gd.t0[3] = t[3];
+      gd.pad[0] = gd.pad[1] = 0;
       groups[g] = gd;
       counts[g] = n;
       offsets[g] = off;
       off += n;
-      tg += mt * nt_gu;
-      td += mt * nt_dn;
+      t[0] += nbig * nt0;
+      t[1] += nsmall * nt1;
+      t[2] += nbig * nt2;
+      t[3] += nsmall * nt3;
     }
     offsets[G] = off;
-    tile_totals[0] = tg;
-    tile_totals[1] = td;
+    for (int i = 0; i < 4; ++i) tile_totals[i] = t[i];
   }
   for (int e = tid; e < E; e += blockDim.x) depth[e] = 0;  // the layer's queues are drained
   const int64_t nk = (int64_t)n_tokens * k;
@@ -107,10 +126,10 @@ __global__ __launch_bounds__(256) void gather_kernel(
 }
 
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int32_t* depth, int32_t* counts,
-                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, int nt_gu,
-                       int nt_dn, int bm, int32_t* pos, float* posw, hipStream_t s) {
+                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, const int* nt,
+                       int big_bm, int small_bm, int32_t* pos, float* posw, hipStream_t s) {
   plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, depth, counts, offsets, groups, tile_totals,
-                                  nt_gu, nt_dn, bm, pos, posw);
+                                  nt[0], nt[1], nt[2], nt[3], big_bm, small_bm, pos, posw);
   return hipGetLastError();
 }
 
