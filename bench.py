@@ -54,6 +54,41 @@ def parse():
     return ap.parse_args()
 
 
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "paper_2505_08944_amd", "csrc")
+
+
+def kernel_source_sha256() -> str:
+    """Hash of every HIP source and header the library is built from: HBM
+    counter readings are only valid for the kernels they were taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def traffic_record(workload: str):
+    """Per-launch HBM bytes of the gate/up kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary of this workload, or None when
+    there is none or the kernels changed since it was taken."""
+    import re
+    path = os.path.join(HERE, "profiles", f"ffn_gate_up_{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    rec = dict(re.findall(r"^(\w+): (\S+)$", txt, re.M))
+    try:
+        if rec["source_sha256"] != kernel_source_sha256():
+            return None
+        return {"bytes": float(rec["hbm_bytes_per_launch"]), "fetch_bytes": float(rec["fetch_bytes_per_launch"]),
+                "write_bytes": float(rec["write_bytes_per_launch"]), "source": os.path.relpath(path, HERE)}
+    except (KeyError, ValueError):
+        return None
+
+
 def copy_calibration(nbytes: int) -> None:
     import torch
     src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
@@ -169,13 +204,25 @@ def main():
 
     # dominant kernel: the gate/up launch (2/3 of the FFN flops)
     gu_flops = 4.0 * w.d * w.f * n_rows          # two GEMMs of 2*d*f flops per row
+    # algorithmic HBM bytes of the launch: gathered rows in, weights of every
+    # expert with rows (gate + up), h rows out
+    wbytes = {"bf16": 2, "fp8": 1, "f32": 4}[w.wdt]
+    abytes = 2 if w.act == "bf16" else 4
+    live = sum(1 for c in counts if c > 0) + w.S
+    gu_bytes = float(n_rows * w.d * abytes + live * 2 * w.f * w.d * wbytes + n_rows * w.f * abytes)
     ffn_flops = 6.0 * w.d * w.f * n_rows
     gu_s = stage_ms["gate_up"] / 1e3
     achieved = gu_flops / gu_s / 1e12
     ffn_s = (stage_ms["gate_up"] + stage_ms["down"]) / 1e3
+    tr = traffic_record(args.workload)
+    kname = "aep::ffn_dlds_kernel<true>" if w.wdt == "bf16" else (
+        "aep::ffn_mfma_kernel<true, true>" if w.wdt == "fp8" else "aep::ffn_f32_kernel<true>")
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                "kernel": "ffn_mfma_kernel<gated> (gate/up launch)",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None if tr is None else tr["bytes"],
+                "kernel": kname + " (gate/up launch)",
+                "traffic_detail": tr,
+                "algorithmic_bytes": gu_bytes,
                 "per_launch": {"flops": gu_flops, "rows": n_rows, "flops_per_row": 4 * w.d * w.f,
                                "avg_ms": round(stage_ms["gate_up"], 4)}}
 
