@@ -69,6 +69,22 @@ __device__ __forceinline__ int c_row(int lane, int r) {
   return ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3);
 }
 
+// Tile order inside one group's nrow x ncol grid of big tiles: panels of
+// kPanel column tiles, row tiles one after another inside a panel, the
+// columns of a row tile adjacent.  The persistent grids hand each XCD runs of
+// consecutive tile ids (32 for 256 workgroups), so an XCD works on a 4 x 8
+// block of tiles: per K step its L2 sees 4 row bands of A and 8 column bands
+// of B instead of every row band of the group against one column band.
+constexpr int kPanel = 8;
+__device__ __forceinline__ void panel_decode(int local, int nrow, int ncol, int& rt, int& ct) {
+  const int per = kPanel * nrow;
+  const int pi = local / per;
+  const int within = local - pi * per;
+  const int w = min(kPanel, ncol - pi * kPanel);  // the last panel may be narrower
+  rt = within / w;
+  ct = pi * kPanel + (within - rt * w);
+}
+
 __device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
   int lo = 0, hi = G;  // t0s[lo] <= tile < t0s[hi]
   while (hi - lo > 1) {
@@ -119,8 +135,10 @@ __global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
     const GroupDesc gd = p.groups[g];
     const WeightDesc wd = p.wtab[g];
     const int local = tile - t0s[g];
-    const int nti = local / gd.nbig;
-    const int m0 = (local - nti * gd.nbig) * kBM;
+    int rt, nti;
+    panel_decode(local, gd.nbig, GATED ? (n_out + kBN / 2 - 1) / (kBN / 2) : (n_out + kBN - 1) / kBN, rt,
+                 nti);
+    const int m0 = rt * kBM;
     const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
 
     // Global sources of this thread's 16-byte chunks: a uniform 64-bit base
@@ -603,13 +621,15 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
   const int nwg = gridDim.x;
   const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
+  const int ncol_big = GATED ? (p.n_out + kBN / 2 - 1) / (kBN / 2) : (p.n_out + kBN - 1) / kBN;
   for (int tile = slot; tile < big_total + small_total; tile += nwg) {
     if (tile < big_total) {
       const int g = find_group(t0b, G, tile);
       const GroupDesc gd = p.groups[g];
       const int local = tile - t0b[g];
-      const int nti = local / gd.nbig;
-      dl_tile<GATED, kBM, kBN, 2>(p, smem, lds_base, gd, p.wtab[g], nti, (local - nti * gd.nbig) * kBM);
+      int rt, nti;
+      panel_decode(local, gd.nbig, ncol_big, rt, nti);
+      dl_tile<GATED, kBM, kBN, 2>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
     } else {
       const int t = tile - big_total;
       const int g = find_group(t0s, G, t);
