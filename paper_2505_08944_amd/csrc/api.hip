@@ -113,8 +113,8 @@ aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE;
 
 // Tiling of the FFN launches: nt[4] = column tiles per row tile (gate/up big,
 // gate/up small, down big, down small) and the row-tile heights.  f32 uses
-// 64 x 64 tiles only; bf16 weights use 256 x 256 tiles plus the 64 x 128
-// small family; fp8 weights use 256 x 256 tiles only.
+// 64 x 64 tiles only; bf16 and fp8 weights use 256 x 256 tiles plus the
+// 64 x 128 small family.
 void tiling(const Ctx& c, int nt[4], int* big_bm, int* small_bm) {
   const int d = c.cfg.d_model, f = c.cfg.d_ffn;
   auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
@@ -129,7 +129,7 @@ void tiling(const Ctx& c, int nt[4], int* big_bm, int* small_bm) {
     nt[2] = cdiv(d, kBN);
     nt[3] = cdiv(d, kSmallBN);
     *big_bm = kBM;
-    *small_bm = c.cfg.w_dtype == AEP_BF16 ? kSmallBM : 0;
+    *small_bm = kSmallBM;
   }
 }
 

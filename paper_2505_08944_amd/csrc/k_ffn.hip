@@ -4,27 +4,28 @@
 //   gate/up:  h[r, c] = silu(x_r . W_gate[c]) * (x_r . W_up[c])   (K = d)
 //   down:     y[r, c] = h_r . W_down[c]                            (K = f)
 //
-// Every group (expert) contributes ceil(n_g / BM) row tiles x (columns / BN)
-// column tiles; the plan kernel laid the tiles of all groups end to end, so
-// one launch covers a whole skewed batch, from a 1-row expert to the hottest
-// one.  Within a group, consecutive tile ids walk the row tiles of one weight
-// column panel, so workgroups running at the same time share that panel.  The
-// workgroup -> tile map is XCD aware: hardware dispatches workgroups round
-// robin over the 8 XCDs, so workgroup w works on slot (w % 8) * (grid / 8) +
-// w / 8, giving each XCD (and its L2) a contiguous run of tiles.
+// The plan kernel laid the tiles of all groups (experts) end to end in two
+// families: 256 x 256 tiles for the full row blocks of hot experts, and
+// 64 x 128 tiles for cold experts and the ragged row tails of hot ones.  One
+// launch covers a whole skewed batch, from a 1-row expert to the hottest one:
+// every big tile first, then the small ones, which also fill the tail of the
+// big family.  The workgroup -> tile map is XCD aware: hardware dispatches
+// workgroups round robin over the 8 XCDs, so workgroup w works on slot
+// (w % 8) * (grid / 8) + w / 8, giving each XCD (and its L2) a contiguous run
+// of tiles, and the big tiles of a group are ordered in panels of 8 column
+// tiles so that such a run is a compact block of row and column tiles.
 //
-// bf16 / fp8-weight path: 256 x 256 output tile per 256-thread workgroup,
-// K step 64, four waves each owning a 128 x 128 quadrant computed with
-// v_mfma_f32_32x32x16_bf16 (f32 accumulate).  Tiles are staged in LDS with a
-// 16-byte row pad (144-byte rows) so the 16-byte fragment reads of 8
-// consecutive rows hit distinct banks; the next K step's global loads are in
-// flight while the current one is multiplied.  Gate/up tiles hold 128
-// features of W_gate and the same 128 of W_up, interleaved per wave quadrant
-// (64 gate rows then 64 up rows), so each lane finds the gate and up
-// accumulator of the same (row, feature) in its own registers and applies the
-// SiLU-and-multiply epilogue without any exchange.  fp8 (OCP e4m3fn) weights
-// are widened to bf16 exactly while being staged into LDS; the per-channel
-// scale multiplies the f32 accumulator in the epilogue.
+// bf16 / fp8-weight path: 256-thread workgroups, K step 64, four waves each
+// owning a quadrant of the tile computed with v_mfma_f32_32x32x16_bf16 (f32
+// accumulate).  Tiles move from global memory straight into LDS (no staging
+// registers) through a ring of stages; the loads of later K steps are in
+// flight while the current one is multiplied.  Gate/up tiles hold BN/2
+// features of W_gate and the same BN/2 of W_up, interleaved per wave quadrant,
+// so each lane finds the gate and up accumulator of the same (row, feature)
+// in its own registers and applies the SiLU-and-multiply epilogue without any
+// exchange.  fp8 (OCP e4m3fn) weights stay fp8 in LDS and are widened to bf16
+// exactly when read into MFMA operands; the per-channel scale multiplies the
+// f32 accumulator in the epilogue.
 //
 // f32 path (f32 activations and weights): 64 x 64 tiles, 4 x 4 outputs per
 // thread with FMA, for the fp32 workload.
@@ -46,22 +47,6 @@ struct FfnParams {
   int K;      // reduction length: d (gate/up) or f (down)
   int n_out;  // output columns: f (gate/up) or d (down)
 };
-
-constexpr int kLds = kBK + 8;  // LDS row stride in bf16 elements (144 bytes)
-
-// 16-byte load through a global (address space 1) pointer, so the compiler
-// emits global_load_dwordx4 rather than a flat load.
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-typedef const __attribute__((address_space(1))) u32x4_t* gptr_u4;
-__device__ __forceinline__ uint4 gload16(const void* p) {
-  const u32x4_t v = *(gptr_u4)(p);
-  uint4 o;
-  o.x = v.x;
-  o.y = v.y;
-  o.z = v.z;
-  o.w = v.w;
-  return o;
-}
 
 // Accumulator layout of v_mfma_f32_32x32x16_bf16: lane l, register r holds
 // column l % 32 and row 8 * (r / 4) + 4 * (l / 32) + r % 4.
@@ -97,291 +82,11 @@ __device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
   return lo;
 }
 
-// 16 fp8 codes -> 16 bf16 (two 16-byte chunks, lowest k first)
-__device__ __forceinline__ void widen_fp8(uint4 v, uint4& lo, uint4& hi) {
-  const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
-  const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
-  lo = make_uint4(a.x, a.y, b.x, b.y);
-  hi = make_uint4(c.x, c.y, d.x, d.y);
-}
-
-constexpr int kStage = (kBM + kBN) * kLds;  // bf16 elements per LDS stage (A tile then B tile)
-constexpr int kEpiLd = 128 + 8;             // epilogue staging row stride (bf16), 272 bytes
-
-template <bool GATED, bool FP8>
-__global__ __launch_bounds__(256, 1) void ffn_mfma_kernel(const FfnParams p) {
-  // Two LDS stages (double buffer) of A and B tiles; reused to stage the
-  // output tile for 16-byte coalesced stores.
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
-  __shared__ int32_t t0s[kMaxGroups + 1];
-
-  constexpr int kBChunks = FP8 ? 4 : 8;  // 16-byte global chunks of B per thread per K step
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int G = p.G;
-  const int total = p.tile_totals[GATED ? 0 : 2];
-  for (int g = tid; g < G; g += 256) t0s[g] = p.groups[g].t0[GATED ? 0 : 2];
-  if (tid == 0) t0s[G] = total;
-  __syncthreads();
-
-  const int nwg = gridDim.x;
-  const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
-  const int K = p.K, KT = K / kBK, n_out = p.n_out;
-  const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
-  uint16_t* O = reinterpret_cast<uint16_t*>(p.out);
-
-  for (int tile = slot; tile < total; tile += nwg) {
-    const int g = find_group(t0s, G, tile);
-    const GroupDesc gd = p.groups[g];
-    const WeightDesc wd = p.wtab[g];
-    const int local = tile - t0s[g];
-    int rt, nti;
-    panel_decode(local, gd.nbig, GATED ? (n_out + kBN / 2 - 1) / (kBN / 2) : (n_out + kBN - 1) / kBN, rt,
-                 nti);
-    const int m0 = rt * kBM;
-    const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
-
-    // Global sources of this thread's 16-byte chunks: a uniform 64-bit base
-    // per operand plus 32-bit element offsets.  Rows beyond the group and
-    // columns beyond the matrix are clamped onto its last row/column, so every
-    // load is in bounds; those rows/columns are never stored.
-    const uint16_t* abase = A + (int64_t)(arow0 + m0) * K;
-    const int alast = gd.n - 1 - m0;
-    uint32_t aoff[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      aoff[i] = (uint32_t)(min((tid >> 3) + 32 * i, alast) * K + (tid & 7) * 8);
-    // B rows of chunk i: bf16 -> tile row (tid >> 3) + 32 i, fp8 -> (tid >> 2) + 64 i.
-    // Gate/up tiles: tile rows [128 w, 128 w + 64) are gate features and
-    // [128 w + 64, 128 w + 128) the same up features (w = wave column), so
-    // the matrix a chunk comes from is fixed by i at compile time.
-    const char* bgate = reinterpret_cast<const char*>(GATED ? wd.gate : wd.down);
-    const char* bup = reinterpret_cast<const char*>(GATED ? wd.up : wd.down);
-    uint32_t boff[kBChunks];
-#pragma unroll
-    for (int i = 0; i < kBChunks; ++i) {
-      int c;
-      if (GATED)
-        c = FP8 ? nti * (kBN / 2) + (i >> 1) * 64 + (tid >> 2)
-                : nti * (kBN / 2) + (i >> 2) * 64 + (i & 1) * 32 + (tid >> 3);
-      else
-        c = FP8 ? nti * kBN + 64 * i + (tid >> 2) : nti * kBN + 32 * i + (tid >> 3);
-      c = min(c, n_out - 1);
-      boff[i] = FP8 ? (uint32_t)(c * K + (tid & 3) * 16) : (uint32_t)(c * K + (tid & 7) * 8);
-    }
-
-    // Two register sets of global-load staging: the loads of step kt + 2
-    // are issued at the start of step kt, so every load has a full K step to
-    // arrive before its data is written to LDS during step kt + 1.
-    uint4 ra0[8], rb0[kBChunks], ra1[8], rb1[kBChunks];
-#define AEP_GLOAD(RA, RB, kt)                                                                    \
-  do {                                                                                           \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) RA[i] = gload16(abase + aoff[i] + (kt) * kBK); \
-    _Pragma("unroll") for (int i = 0; i < kBChunks; ++i) {                                       \
-      const bool up_ = GATED && (FP8 ? (i & 1) : ((i >> 1) & 1));                                \
-      RB[i] = gload16((up_ ? bup : bgate) + ((size_t)boff[i] + (size_t)(kt) * kBK) * (FP8 ? 1 : 2)); \
-    }                                                                                            \
-  } while (0)
-#define AEP_LSTORE(RA, RB, st)                                                                   \
-  do {                                                                                           \
-    uint16_t* As_ = smem + (st) * kStage;                                                        \
-    uint16_t* Bs_ = As_ + kBM * kLds;                                                            \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                                \
-        *reinterpret_cast<uint4*>(&As_[((tid >> 3) + 32 * i) * kLds + (tid & 7) * 8]) = RA[i];    \
-    if constexpr (FP8) {                                                                         \
-      _Pragma("unroll") for (int i = 0; i < kBChunks; ++i) {                                     \
-        uint16_t* dst_ = &Bs_[((tid >> 2) + 64 * i) * kLds + (tid & 3) * 16];                    \
-        uint4 lo_, hi_;                                                                          \
-        widen_fp8(RB[i], lo_, hi_);                                                              \
-        *reinterpret_cast<uint4*>(dst_) = lo_;                                                   \
-        *reinterpret_cast<uint4*>(dst_ + 8) = hi_;                                               \
-      }                                                                                          \
-    } else {                                                                                     \
-      _Pragma("unroll") for (int i = 0; i < kBChunks; ++i)                                       \
-          *reinterpret_cast<uint4*>(&Bs_[((tid >> 3) + 32 * i) * kLds + (tid & 7) * 8]) = RB[i];  \
-    }                                                                                            \
-  } while (0)
-  constexpr int kStores = 8 + (FP8 ? 2 * kBChunks : kBChunks);  // LDS writes per thread per step
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-#define AEP_READ(Abuf, ks_, A_, B_)                                                              \
-  do {                                                                                           \
-    const uint16_t* As_ = (Abuf);                                                                \
-    const uint16_t* Bs_ = As_ + kBM * kLds;                                                      \
-    const int kof_ = (ks_) * 16 + (lane >> 5) * 8;                                               \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) A_[i] =                                        \
-        *reinterpret_cast<const bf16x8_t*>(&As_[(wm * 128 + i * 32 + (lane & 31)) * kLds + kof_]); \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j) B_[j] =                                        \
-        *reinterpret_cast<const bf16x8_t*>(&Bs_[(wn * 128 + j * 32 + (lane & 31)) * kLds + kof_]); \
-  } while (0)
-#define AEP_MMA(A_, B_)                                                                          \
-  do {                                                                                           \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i) _Pragma("unroll") for (int j = 0; j < 4; ++j)  \
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i], B_[j], acc[i][j], 0, 0, 0);   \
-  } while (0)
-// One software-pipeline group: read the operands of the next 16-wide k slice
-// (8 LDS reads) while the 16 MFMAs of the current slice run.  Reads are
-// spread two per four MFMAs: bunching them costs MFMA issue slots (measured
-// on gfx950: 8 reads then 16 MFMAs runs ~10% slower than 2 : 4).
-#define AEP_GROUP(Abuf, ks_, An, Bn, Ac, Bc)                                                     \
-  do {                                                                                           \
-    AEP_READ(Abuf, ks_, An, Bn);                                                                 \
-    AEP_MMA(Ac, Bc);                                                                             \
-    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                         \
-    }                                                                                            \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
-  } while (0)
-// The same, with the global loads of step kt + 2 spread between the MFMAs.
-#define AEP_GROUP_LD(Abuf, ks_, An, Bn, Ac, Bc, RA, RB, kl)                                      \
-  do {                                                                                           \
-    AEP_GLOAD(RA, RB, kl);                                                                       \
-    AEP_READ(Abuf, ks_, An, Bn);                                                                 \
-    AEP_MMA(Ac, Bc);                                                                             \
-    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
-      __builtin_amdgcn_sched_group_barrier(0x020, (8 + kBChunks) / 4, 0);                        \
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                         \
-    }                                                                                            \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
-  } while (0)
-// The same, with the LDS writes of the next step's tile spread between the MFMAs.
-#define AEP_GROUP_ST(Abuf, ks_, An, Bn, Ac, Bc, RA, RB, st)                                      \
-  do {                                                                                           \
-    AEP_READ(Abuf, ks_, An, Bn);                                                                 \
-    AEP_LSTORE(RA, RB, st);                                                                      \
-    AEP_MMA(Ac, Bc);                                                                             \
-    _Pragma("unroll") for (int q_ = 0; q_ < 4; ++q_) {                                           \
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x200, kStores / 16, 0);                              \
-    }                                                                                            \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
-  } while (0)
-// One K step (64 deep = four 16-wide slices) over LDS stage kt & 1:
-//   issue the global loads of step kt + 2; slice 0 runs while slice 1 is
-//   read; slice 1 runs while slice 2 is read and the tile of step kt + 1
-//   (loaded during step kt - 1) is written to the other LDS stage; slice 2
-//   runs while slice 3 is read; barrier; slice 3 runs while slice 0 of the
-//   next stage is read.  The other stage was last read during step kt - 1,
-//   before that step's barrier.  Past the last step, loads and stores repeat
-//   the last step's data (kept unconditional so they stay in registers).
-#define AEP_STEP(kt_, RLa, RLb, RSa, RSb)                                                        \
-  do {                                                                                           \
-    const uint16_t* cur_ = smem + ((kt_) & 1) * kStage;                                          \
-    const uint16_t* nxt_ = smem + (((kt_) + 1) & 1) * kStage;                                    \
-    AEP_GROUP_LD(cur_, 1, a1, b1, a0, b0, RLa, RLb, min((kt_) + 2, KT - 1));                     \
-    AEP_GROUP_ST(cur_, 2, a0, b0, a1, b1, RSa, RSb, ((kt_) + 1) & 1);                            \
-    AEP_GROUP(cur_, 3, a1, b1, a0, b0);                                                          \
-    __syncthreads();                                                                             \
-    AEP_GROUP(nxt_, 0, a0, b0, a1, b1);                                                          \
-  } while (0)
-
-    bf16x8_t a0[4], b0[4], a1[4], b1[4];
-    AEP_GLOAD(ra0, rb0, 0);
-    AEP_GLOAD(ra1, rb1, min(1, KT - 1));
-    __syncthreads();  // every wave is done with the previous tile's LDS
-    AEP_LSTORE(ra0, rb0, 0);
-    __syncthreads();
-    AEP_READ(smem, 0, a0, b0);
-    int kt = 0;
-    for (; kt + 1 < KT; kt += 2) {
-      AEP_STEP(kt, ra0, rb0, ra1, rb1);
-      AEP_STEP(kt + 1, ra1, rb1, ra0, rb0);
-    }
-    if (kt < KT) AEP_STEP(kt, ra0, rb0, ra1, rb1);
-#undef AEP_STEP
-#undef AEP_GROUP_ST
-#undef AEP_GROUP_LD
-#undef AEP_GROUP
-#undef AEP_MMA
-#undef AEP_READ
-#undef AEP_GLOAD
-#undef AEP_LSTORE
-
-    // Epilogue: stage bf16 results in LDS ([256][128 + 8]), then write
-    // 16-byte chunks of whole rows.  Gate/up tiles produce 128 features in
-    // one pass; down tiles produce 256 columns in two passes of 128 (column
-    // blocks j = 0, 1 then j = 2, 3 of every wave).
-    uint16_t* Cs = smem;
-    constexpr int kPasses = GATED ? 1 : 2;
-#pragma unroll
-    for (int pass = 0; pass < kPasses; ++pass) {
-      if (pass) __syncthreads();  // previous pass's reads are done
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int j = GATED ? jj : 2 * pass + jj;
-        const int cl = wn * 64 + jj * 32 + (lane & 31);  // column inside the staged 128
-        float sg = 1.f, su = 1.f;
-        if constexpr (FP8) {
-          if constexpr (GATED) {
-            const int fc = min(nti * (kBN / 2) + cl, n_out - 1);
-            sg = __uint_as_float((uint32_t)wd.s_gu[fc] << 16);
-            su = __uint_as_float((uint32_t)wd.s_gu[n_out + fc] << 16);
-          } else {
-            const int cc = min(nti * kBN + wn * 128 + j * 32 + (lane & 31), n_out - 1);
-            sg = __uint_as_float((uint32_t)wd.s_down[cc] << 16);
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int rl = wm * 128 + i * 32 + c_row(lane, r);
-            float v;
-            if constexpr (GATED) {
-              const float gv = acc[i][j][r] * sg;
-              const float uv = acc[i][j + 2][r] * su;
-              v = __fdividef(gv, 1.f + __expf(-gv)) * uv;
-            } else {
-              v = acc[i][j][r] * sg;
-            }
-            Cs[rl * kEpiLd + cl] = (uint16_t)f32_to_bf16_rne(v);
-          }
-        }
-      }
-      __syncthreads();
-      // 256 rows x 16 chunks of 8 columns; chunk c < 8 is wave column 0's
-      // block, c >= 8 wave column 1's.
-#pragma unroll 4
-      for (int it = 0; it < 16; ++it) {
-        const int q = tid + 256 * it;
-        const int rl = q >> 4, c16 = q & 15;
-        const int row = m0 + rl;
-        int col;
-        if (GATED)
-          col = nti * (kBN / 2) + c16 * 8;
-        else
-          col = nti * kBN + (c16 >> 3) * 128 + pass * 64 + (c16 & 7) * 8;
-        if (row < gd.n && col < n_out) {
-          const uint4 v = *reinterpret_cast<const uint4*>(&Cs[rl * kEpiLd + c16 * 8]);
-          *reinterpret_cast<uint4*>(O + (int64_t)(gd.y_row0 + row) * n_out + col) = v;
-        }
-      }
-    }
-  }
-}
-
-// ------------------------------------------------- bf16 weights: direct-to-LDS
-// The same 256 x 256 tiles and quadrant MFMA work, but tiles move from global
-// memory straight into LDS (global_load_lds_dwordx4: 64 lanes x 16 bytes into
-// 1 KB of consecutive LDS, no staging registers), through a ring of STAGES
-// LDS buffers with a prefetch distance of STAGES - 1 K steps of BKS.  LDS
-// rows are not padded; a 16-byte chunk c of tile row r sits at position
+// ------------------------------------------------- direct-to-LDS MFMA tiles
+// Tiles move from global memory straight into LDS (global_load_lds_dwordx4:
+// 64 lanes x 16 bytes into 1 KB of consecutive LDS, no staging registers),
+// through a ring of STAGES LDS buffers with a prefetch distance of
+// STAGES - 1 K steps.  LDS rows are not padded; a 16-byte chunk c of tile row r sits at position
 // c ^ s(r), where s spreads the 8 rows read together by one fragment read
 // over distinct banks (s(r) = r % 8 for 128-byte rows, (r / 2) % 4 for
 // 64-byte rows).  Each lane picks the global chunk that belongs at its fixed
@@ -410,62 +115,82 @@ __device__ __forceinline__ void wait_vmcnt() {
 // One output tile of BM rows x BN columns (gate/up: BN/2 features of gate and
 // the same BN/2 of up) at row m0 of group gd, column tile nti.  Four waves in
 // a 2 x 2 grid, each owning a (BM/2) x (BN/2) block of 32 x 32 MFMA
-// fragments.  STAGES LDS buffers of (BM + BN) x 128 bytes form the ring
-// (prefetch distance STAGES - 1 K steps of 64).
-template <bool GATED, int BM, int BN, int STAGES>
+// fragments.  STAGES LDS buffers form the ring (prefetch distance STAGES - 1
+// K steps of 64); a stage holds the A tile (BM rows x 128 bytes, bf16) and
+// the B tile (BN rows x 128 bytes for bf16 weights, x 64 bytes for fp8).
+//
+// fp8 weights (FP8): B stays e4m3 in LDS.  One 16-byte read gives a lane 16
+// consecutive k of its row; lanes 0-31 read k-chunk 2m, lanes 32-63 chunk
+// 2m + 1 (K elements 32m .. 32m + 31), and the two halves of the read feed
+// two MFMAs after an exact e4m3 -> bf16 conversion.  The A reads follow the
+// same assignment of k to lanes (bf16 chunks 4m + 2h and 4m + 2h + 1 for
+// lane half h), so every MFMA still pairs equal k; per-channel scales are
+// applied in the epilogue.
+template <bool GATED, bool FP8, int BM, int BN, int STAGES, int CAP>
 __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem, uint32_t lds_base,
                                         const GroupDesc& gd, const WeightDesc& wd, int nti, int m0) {
   constexpr int BKS = kBK;
-  constexpr int kRowB = BKS * 2;              // 128 bytes: one tile row of one K step
+  constexpr int kRowA = BKS * 2;              // 128 bytes: one A row of one K step
+  constexpr int kRowB = FP8 ? BKS : BKS * 2;  // one B row of one K step
+  constexpr int kRplA = 1024 / kRowA;         // rows per direct load (8)
+  constexpr int kRplB = 1024 / kRowB;         // 8, or 16 for fp8
+  constexpr int kChB = kRowB / 16;            // 16-byte chunks per B row (8 or 4)
   constexpr int TM = BM / 2, TN = BN / 2;     // wave tile
   constexpr int MI = TM / 32, NI = TN / 32;   // 32 x 32 fragments per wave
-  constexpr int kNA = BM / 8 / 4;             // direct loads per wave per K step: A (8 rows each)
-  constexpr int kNB = BN / 8 / 4;             // ... and B
-  constexpr int kTileA = BM * kRowB, kStageB = (BM + BN) * kRowB;
+  constexpr int kNA = BM / kRplA / 4;         // direct loads per wave per K step: A
+  constexpr int kNB = BN / kRplB / 4;         // ... and B
+  constexpr int kTileA = BM * kRowA, kStageB = BM * kRowA + BN * kRowB;
   constexpr int kDist = STAGES - 1;
   constexpr int kPerStep = kNA + kNB;
   constexpr int kLd = BN / 2 + 8;             // epilogue staging row stride (bf16)
   static_assert(MI >= 1 && NI >= 2 && NI % 2 == 0, "wave tile");
-  static_assert(STAGES * kStageB <= 2 * (kBM + kBN) * kRowB, "ring must fit the shared buffer");
-  static_assert(BM * kLd * 2 <= 2 * (kBM + kBN) * kRowB, "epilogue staging must fit");
+  static_assert(kNA >= 1 && kNB >= 1, "loads per wave");
+  static_assert(!GATED || kNB * kRplB == TN / 2, "a wave's B rows are all gate or all up rows");
+  static_assert(STAGES * kStageB <= CAP, "ring must fit the shared buffer");
+  static_assert(BM * kLd * 2 <= CAP, "epilogue staging must fit");
+  static_assert((kDist - 1) * kPerStep < 64, "vmcnt range");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int K = p.K, KT = K / BKS, n_out = p.n_out;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
   uint16_t* O = reinterpret_cast<uint16_t*>(p.out);
-  // loader: lane l fills LDS position l % 8 of row l / 8 of an 8-row block with
-  // the k chunk that belongs there, (l % 8) ^ (row % 8)
-  const int ld_row = lane >> 3;
-  const int ld_c = (lane & 7) ^ (lane >> 3);
-  // reader: fragment row and its swizzle
+  // chunk swizzles: spread the 8 rows one 128-byte bank window sees over
+  // distinct banks (r % 8 for 128-byte rows, (r / 2) % 4 for 64-byte rows)
+  auto swz_b = [](int r) { return kChB == 8 ? (r & 7) : ((r >> 1) & 3); };
+  // loaders: lane l fills chunk position l % chunks-per-row of row
+  // l / chunks-per-row of a load block with the global chunk that belongs
+  // there (load blocks start at multiples of 8 or 16 rows)
+  const int lda_row = lane >> 3;
+  const int lda_c = (lane & 7) ^ lda_row;
+  const int ldb_row = lane / kChB;
+  const int ldb_c = (lane % kChB) ^ swz_b(ldb_row);
+  // readers: fragment row and its swizzle
   const int rd_row = lane & 31;
-  const int rd_s = rd_row & 7;
+  const int rd_sa = rd_row & 7;
+  const int rd_sb = swz_b(rd_row);
 
   const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
   const uint16_t* abase = A + (int64_t)(arow0 + m0) * K;
   const int alast = gd.n - 1 - m0;
   uint32_t aoff[kNA], boff[kNB];
 #pragma unroll
-  for (int i = 0; i < kNA; ++i) aoff[i] = (uint32_t)(min((wave * kNA + i) * 8 + ld_row, alast) * K + ld_c * 8);
+  for (int i = 0; i < kNA; ++i)
+    aoff[i] = (uint32_t)(min((wave * kNA + i) * kRplA + lda_row, alast) * K + lda_c * 8);
   // B rows: a wave column's TN rows are TN/2 gate features then the same TN/2
-  // up features; an 8-row load block never straddles the two halves.
-  const uint16_t* bsrc[kNB];
+  // up features; a wave's B rows lie in one of the two halves.
+  const unsigned char* bmat;
+  {
+    const int br0 = wave * kNB * kRplB;
+    const bool up = GATED && (br0 % TN) >= TN / 2;
+    bmat = reinterpret_cast<const unsigned char*>(GATED ? (up ? wd.up : wd.gate) : wd.down);
+  }
 #pragma unroll
   for (int i = 0; i < kNB; ++i) {
-    const int br = (wave * kNB + i) * 8 + ld_row;
-    int c;
-    bool up = false;
-    if (GATED) {
-      const int within = br % TN;
-      up = within >= TN / 2;
-      c = nti * (BN / 2) + (br / TN) * (TN / 2) + within % (TN / 2);
-    } else {
-      c = nti * BN + br;
-    }
+    const int br = (wave * kNB + i) * kRplB + ldb_row;
+    int c = GATED ? nti * (BN / 2) + (br / TN) * (TN / 2) + (br % TN) % (TN / 2) : nti * BN + br;
     c = min(c, n_out - 1);
-    boff[i] = (uint32_t)(c * K + ld_c * 8);
-    bsrc[i] = reinterpret_cast<const uint16_t*>(GATED ? (up ? wd.up : wd.gate) : wd.down);
+    boff[i] = (uint32_t)(c * K * (FP8 ? 1 : 2) + ldb_c * 16);  // bytes
   }
 
 #define DL_LOAD(kt_, st_)                                                                        \
@@ -475,16 +200,42 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     _Pragma("unroll") for (int i = 0; i < kNA; ++i)                                              \
         dload16(abase + aoff[i] + (kt_) * BKS, sa_ + i * 1024);                                  \
     _Pragma("unroll") for (int i = 0; i < kNB; ++i)                                              \
-        dload16(bsrc[i] + boff[i] + (kt_) * BKS, sb_ + i * 1024);                                \
+        dload16(bmat + boff[i] + (kt_) * kRowB, sb_ + i * 1024);                                 \
   } while (0)
+  // bf16 weights: k-slice ks (16 k) of every fragment
 #define DL_READ(st_, ks_, A_, B_)                                                                \
   do {                                                                                           \
     const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
-    const int ro_ = rd_row * kRowB + (((2 * (ks_) + (lane >> 5)) ^ rd_s) << 4);                  \
+    const int ro_ = rd_row * kRowA + (((2 * (ks_) + (lane >> 5)) ^ rd_sa) << 4);                 \
     _Pragma("unroll") for (int i = 0; i < MI; ++i) A_[i] =                                       \
-        *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + i * 32) * kRowB + ro_);              \
+        *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + i * 32) * kRowA + ro_);              \
     _Pragma("unroll") for (int j = 0; j < NI; ++j) B_[j] =                                       \
         *reinterpret_cast<const bf16x8_t*>(ab_ + kTileA + (wn * TN + j * 32) * kRowB + ro_);     \
+  } while (0)
+  // fp8 weights: half-step m (32 k): A for both MFMAs, raw e4m3 B
+#define DL_READ8(st_, m_, A1_, A2_, R_)                                                          \
+  do {                                                                                           \
+    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
+    const int ca_ = 4 * (m_) + 2 * (lane >> 5);                                                  \
+    const int ra1_ = rd_row * kRowA + ((ca_ ^ rd_sa) << 4);                                      \
+    const int ra2_ = rd_row * kRowA + (((ca_ + 1) ^ rd_sa) << 4);                                \
+    const int rb_ = rd_row * kRowB + (((2 * (m_) + (lane >> 5)) ^ rd_sb) << 4);                  \
+    _Pragma("unroll") for (int j = 0; j < NI; ++j) R_[j] =                                       \
+        *reinterpret_cast<const uint4*>(ab_ + kTileA + (wn * TN + j * 32) * kRowB + rb_);        \
+    _Pragma("unroll") for (int i = 0; i < MI; ++i) {                                             \
+      A1_[i] = *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + i * 32) * kRowA + ra1_);      \
+      A2_[i] = *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + i * 32) * kRowA + ra2_);      \
+    }                                                                                            \
+  } while (0)
+  // e4m3 x 16 -> two bf16 x 8 operands (exact)
+#define DL_WIDEN(R_, B1_, B2_)                                                                   \
+  do {                                                                                           \
+    _Pragma("unroll") for (int j = 0; j < NI; ++j) {                                             \
+      const uint2 w0_ = e4m3x4_to_bf16x4(R_[j].x), w1_ = e4m3x4_to_bf16x4(R_[j].y);              \
+      const uint2 w2_ = e4m3x4_to_bf16x4(R_[j].z), w3_ = e4m3x4_to_bf16x4(R_[j].w);              \
+      B1_[j] = __builtin_bit_cast(bf16x8_t, make_uint4(w0_.x, w0_.y, w1_.x, w1_.y));             \
+      B2_[j] = __builtin_bit_cast(bf16x8_t, make_uint4(w2_.x, w2_.y, w3_.x, w3_.y));             \
+    }                                                                                            \
   } while (0)
 #define DL_MMA(A_, B_)                                                                           \
   do {                                                                                           \
@@ -503,6 +254,21 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
   } while (0)
+  // fp8: widen the raw B read in the previous group, then read the next
+  // half-step while the MFMAs of this one run
+#define DL_GROUP8(st_, m_, A1n, A2n, Rn, A1c, A2c, Rc)                                           \
+  do {                                                                                           \
+    DL_WIDEN(Rc, b1, b2);                                                                        \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+    DL_READ8(st_, m_, A1n, A2n, Rn);                                                             \
+    DL_MMA(A1c, b1);                                                                             \
+    DL_MMA(A2c, b2);                                                                             \
+    _Pragma("unroll") for (int q_ = 0; q_ < 2 * kQ; ++q_) {                                      \
+      __builtin_amdgcn_sched_group_barrier(0x100, (2 * MI + NI + 2 * kQ - 1) / (2 * kQ), 0);     \
+      __builtin_amdgcn_sched_group_barrier(0x008, MI * NI / kQ, 0);                              \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+  } while (0)
 
   f32x16_t acc[MI][NI];
 #pragma unroll
@@ -512,7 +278,6 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
   // Nothing of this wave may still be in flight when the ring is refilled
   // (the wait counter is in issue order, so earlier stores of the previous
   // tile's epilogue would otherwise blur the counts below).
@@ -522,26 +287,48 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   for (int s = 0; s < kDist; ++s) DL_LOAD(min(s, KT - 1), s);
   wait_vmcnt<(kDist - 1) * kPerStep>();  // step 0 has landed (this wave's part)
   __syncthreads();                       // ... and every wave's part
-  DL_READ(0, 0, a0, b0);
   // Step kt computes stage kt % STAGES and refills the stage read in step
   // kt - 1 (every wave passed that step's barrier) with step kt + kDist.
   // Past the last step the loads repeat the last step (never read).
-  int st = 0;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int nst = st + 1 == STAGES ? 0 : st + 1;
-    const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
-    DL_LOAD(min(kt + kDist, KT - 1), fst);
-    __builtin_amdgcn_sched_barrier(0);
-    DL_GROUP(st, 1, a1, b1, a0, b0);
-    DL_GROUP(st, 2, a0, b0, a1, b1);
-    DL_GROUP(st, 3, a1, b1, a0, b0);
-    wait_vmcnt<(kDist - 1) * kPerStep>();  // step kt + 1 has landed
-    __syncthreads();
-    DL_GROUP(nst, 0, a0, b0, a1, b1);
-    st = nst;
+  if constexpr (!FP8) {
+    bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
+    DL_READ(0, 0, a0, b0);
+    int st = 0;
+    for (int kt = 0; kt < KT; ++kt) {
+      const int nst = st + 1 == STAGES ? 0 : st + 1;
+      const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
+      DL_LOAD(min(kt + kDist, KT - 1), fst);
+      __builtin_amdgcn_sched_barrier(0);
+      DL_GROUP(st, 1, a1, b1, a0, b0);
+      DL_GROUP(st, 2, a0, b0, a1, b1);
+      DL_GROUP(st, 3, a1, b1, a0, b0);
+      wait_vmcnt<(kDist - 1) * kPerStep>();  // step kt + 1 has landed
+      __syncthreads();
+      DL_GROUP(nst, 0, a0, b0, a1, b1);
+      st = nst;
+    }
+  } else {
+    bf16x8_t a10[MI], a20[MI], a11[MI], a21[MI], b1[NI], b2[NI];
+    uint4 r0[NI], r1[NI];
+    DL_READ8(0, 0, a10, a20, r0);
+    int st = 0;
+    for (int kt = 0; kt < KT; ++kt) {
+      const int nst = st + 1 == STAGES ? 0 : st + 1;
+      const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
+      DL_LOAD(min(kt + kDist, KT - 1), fst);
+      __builtin_amdgcn_sched_barrier(0);
+      DL_GROUP8(st, 1, a11, a21, r1, a10, a20, r0);
+      wait_vmcnt<(kDist - 1) * kPerStep>();  // step kt + 1 has landed
+      __syncthreads();
+      DL_GROUP8(nst, 0, a10, a20, r0, a11, a21, r1);
+      st = nst;
+    }
   }
+#undef DL_GROUP8
 #undef DL_GROUP
 #undef DL_MMA
+#undef DL_WIDEN
+#undef DL_READ8
 #undef DL_READ
 #undef DL_LOAD
 
@@ -549,6 +336,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // chunks of whole rows.  Gate/up: one pass, feature fragment j pairs with
   // up fragment j + NI/2.  Down: two passes of BN/2 columns (each wave
   // contributes column fragments pass * NI/2 .. pass * NI/2 + NI/2 - 1).
+  // fp8 weights: the per-channel scales multiply the accumulators here.
   // The loads issued past the last step target the ring this reuses: let
   // them land first.
   wait_vmcnt<0>();
@@ -562,6 +350,17 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     for (int jj = 0; jj < NI / 2; ++jj) {
       const int j = GATED ? jj : pass * (NI / 2) + jj;
       const int cl = wn * (TN / 2) + jj * 32 + (lane & 31);
+      float sg = 1.f, su = 1.f;
+      if constexpr (FP8) {
+        if constexpr (GATED) {
+          const int fc = min(nti * (BN / 2) + cl, n_out - 1);
+          sg = __uint_as_float((uint32_t)wd.s_gu[fc] << 16);
+          su = __uint_as_float((uint32_t)wd.s_gu[n_out + fc] << 16);
+        } else {
+          const int cc = min(nti * BN + wn * TN + j * 32 + (lane & 31), n_out - 1);
+          sg = __uint_as_float((uint32_t)wd.s_down[cc] << 16);
+        }
+      }
 #pragma unroll
       for (int i = 0; i < MI; ++i) {
 #pragma unroll
@@ -569,10 +368,11 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
           const int rl = wm * TM + i * 32 + c_row(lane, r);
           float v;
           if constexpr (GATED) {
-            const float gv = acc[i][j][r];
-            v = __fdividef(gv, 1.f + __expf(-gv)) * acc[i][j + NI / 2][r];
+            const float gv = FP8 ? acc[i][j][r] * sg : acc[i][j][r];
+            const float uv = FP8 ? acc[i][j + NI / 2][r] * su : acc[i][j + NI / 2][r];
+            v = __fdividef(gv, 1.f + __expf(-gv)) * uv;
           } else {
-            v = acc[i][j][r];
+            v = FP8 ? acc[i][j][r] * sg : acc[i][j][r];
           }
           Cs[rl * kLd + cl] = (uint16_t)f32_to_bf16_rne(v);
         }
@@ -595,15 +395,24 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   }
 }
 
-// bf16-weight FFN launch: every tile of the big family (256 rows), then every
-// tile of the small family (64 rows: cold experts and the ragged tails of hot
-// ones), in one persistent grid.  Small tiles come last, so they also fill
-// the tail of the big ones.  Small tiles are 64 rows x 128 columns: cold
-// experts are weight-streaming bound, and narrower tiles spread each expert's
-// weights over more CUs.
-template <bool GATED>
+// The FFN launch for bf16 or fp8 weights: every tile of the big family (256
+// rows), then every tile of the small family (64 rows: cold experts and the
+// ragged tails of hot ones), in one persistent grid.  Small tiles come last,
+// so they also fill the tail of the big ones.  Small tiles are 64 rows x 128
+// columns: cold experts are weight-streaming bound, and narrower tiles spread
+// each expert's weights over more CUs.  fp8 stages are smaller (e4m3 B
+// tiles), so the rings are deeper: 3 big / 6 small stages instead of 2 / 4.
+template <bool FP8>
+constexpr int ring_bytes(int stages, int bm, int bn) {
+  return stages * (bm * kBK * 2 + bn * kBK * (FP8 ? 1 : 2));
+}
+template <bool GATED, bool FP8>
 __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * (kBM + kBN) * kBK * 2];
+  constexpr int kBigStages = FP8 ? 3 : 2, kSmallStages = FP8 ? 6 : 4;
+  constexpr int kRingBig = ring_bytes<FP8>(kBigStages, kBM, kBN);
+  constexpr int kRingSmall = ring_bytes<FP8>(kSmallStages, kSmallBM, kSmallBN);
+  constexpr int kRing = kRingBig > kRingSmall ? kRingBig : kRingSmall;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kRing];
   __shared__ int32_t t0b[kMaxGroups + 1], t0s[kMaxGroups + 1];
   const int tid = threadIdx.x;
   const int G = p.G;
@@ -629,15 +438,15 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const int local = tile - t0b[g];
       int rt, nti;
       panel_decode(local, gd.nbig, ncol_big, rt, nti);
-      dl_tile<GATED, kBM, kBN, 2>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
+      dl_tile<GATED, FP8, kBM, kBN, kBigStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
     } else {
       const int t = tile - big_total;
       const int g = find_group(t0s, G, t);
       const GroupDesc gd = p.groups[g];
       const int local = t - t0s[g];
       const int nti = local / gd.nsmall;
-      dl_tile<GATED, kSmallBM, kSmallBN, 4>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                  gd.small_row0 + (local - nti * gd.nsmall) * kSmallBM);
+      dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kRing>(
+          p, smem, lds_base, gd, p.wtab[g], nti, gd.small_row0 + (local - nti * gd.nsmall) * kSmallBM);
     }
   }
 }
@@ -758,14 +567,14 @@ hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* gr
   const int grid = grid_for(max_tiles, num_cu);  // one 256-thread workgroup per CU (LDS, registers)
   if (w_dtype == 2) {
     if (stage == 0)
-      ffn_mfma_kernel<true, true><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<true, true><<<grid, 256, 0, s>>>(p);
     else
-      ffn_mfma_kernel<false, true><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<false, true><<<grid, 256, 0, s>>>(p);
   } else {
     if (stage == 0)
-      ffn_dlds_kernel<true><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<true, false><<<grid, 256, 0, s>>>(p);
     else
-      ffn_dlds_kernel<false><<<grid, 256, 0, s>>>(p);
+      ffn_dlds_kernel<false, false><<<grid, 256, 0, s>>>(p);
   }
   return hipGetLastError();
 }

@@ -30,6 +30,11 @@ SMALL = {
     "mid_e64": W("mid_e64", 104, d=128, f=192, E=64, k=6, zipf_s=1.1, tokens=(33,), n_frag=1),
     # fp8 weights through the router
     "mid_fp8": W("mid_fp8", 105, d=384, f=512, E=8, k=2, zipf_s=1.2, wdt="fp8", tokens=(530,), n_frag=2),
+    # fp8 with K shorter than the prefetch distance of the small-tile ring
+    # (d = 128: 2 K steps; f = 192: 3 K steps, ragged gate/up columns) and a
+    # shared expert
+    "short_fp8": W("short_fp8", 106, d=128, f=192, E=8, S=1, k=2, zipf_s=1.2, wdt="fp8", tokens=(300,),
+                   n_frag=2),
 }
 
 
