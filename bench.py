@@ -215,8 +215,8 @@ def main():
     achieved = gu_flops / gu_s / 1e12
     ffn_s = (stage_ms["gate_up"] + stage_ms["down"]) / 1e3
     tr = traffic_record(args.workload)
-    kname = "aep::ffn_dlds_kernel<true>" if w.wdt == "bf16" else (
-        "aep::ffn_mfma_kernel<true, true>" if w.wdt == "fp8" else "aep::ffn_f32_kernel<true>")
+    kname = {"bf16": "aep::ffn_dlds_kernel<true, false>", "fp8": "aep::ffn_dlds_kernel<true, true>"}.get(
+        w.wdt, "aep::ffn_f32_kernel<true>")
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if tr is None else tr["bytes"],
