@@ -168,6 +168,90 @@ aep_status aep_expert_counts(void* ctx, int32_t layer, int32_t* h_counts, void* 
 aep_status aep_pick_layer(const void* ctx, int32_t policy, double delta, int32_t lookahead,
                           int32_t* layer);
 
+/* Scheduler over (block, expert) queues (Sec. 3.4, Algorithm 1), host only:
+ * pick the queue to run next from a host table Q [n_blocks][n_experts] of
+ * queued rows (row-major, every entry >= 0).
+ *  MTFS:   the largest queue.
+ *  FLFS:   the lowest block holding any row; its largest queue.
+ *  DEFRAG: Algorithm 1: score(b, e) = Q[b][e] + sum_{i=1..lookahead}
+ *          (sum_e' Q[(b+i) mod n_blocks][e'] / n_experts) * delta^i over the
+ *          non-empty queues (delta >= 0, lookahead >= 0).
+ * Ties go to the lowest (block, expert) in row-major order.  AEP_ERR_EMPTY
+ * (outputs untouched) when every queue is empty. */
+aep_status aep_sched_pick(const int64_t* Q, int32_t n_blocks, int32_t n_experts, int32_t policy,
+                          double delta, int32_t lookahead, int32_t* block, int32_t* expert);
+
+/* Discrete-event model of one expert runtime (Sec. 3.4 behaviour, Sec. 5
+ * arrivals), host only.  One GPU hosts every expert of every block.  Request r
+ * sends its first token to block 0 at arrival_us[r]; a token queued at block b
+ * is routed to top_k distinct experts drawn from the integer popularity CDF
+ * (one row per expert queue).  When the GPU is free and rows are queued (and
+ * the time is before horizon_us) the policy picks one (block, expert) queue
+ * (granularity 0, aep_sched_pick) or a whole block (granularity 1,
+ * aep_pick_layer's scores over block totals) and drains it; the step takes
+ * (non-empty experts) * cost_fixed_us + ceil(rows * cost_row_ns / 1000) us.
+ * When it ends, each token whose last queued row of that block ran leaves:
+ * the tokens that leave in one step are spread over n_frag attention ranks,
+ * and each rank's fragment reaches the next block (after the last block:
+ * block 0 with the request's next token, unless the request has produced
+ * out_len[r] tokens and completes) attn_us + jitter later, jitter drawn in
+ * [0, jitter_us].  Random choices use the SplitMix64 output function on
+ * seed + stream * 0xD1B54A32D192ED03 + counter * 0x9E3779B97F4A7C15 (mod 2^64),
+ * streams 1 routing (counter ((r * 2^20 + it) * 2^12 + block) * 2^12 + draw),
+ * 2 fragment (counter (r * 2^20 + it) * 2^12 + block), 3 jitter (counter
+ * step * 2^12 + rank); times are integer microseconds, so runs are exactly
+ * reproducible.  All pointers are host memory owned by the caller. */
+typedef struct {
+  int32_t n_blocks;           /* N_B: 1..4096                                      */
+  int32_t n_experts;          /* N_E experts per block: 1..4096                    */
+  int32_t top_k;              /* 1..min(N_E, 64)                                   */
+  int32_t n_frag;             /* attention ranks: 1..4096                          */
+  int32_t granularity;        /* 0: (block, expert) queues; 1: whole blocks        */
+  int32_t policy;             /* aep_policy                                        */
+  double delta;               /* DEFRAG weight decay, >= 0                         */
+  int32_t lookahead;          /* DEFRAG lookahead depth, >= 0                      */
+  int32_t n_requests;         /* 0..2^20                                           */
+  int64_t attn_us;            /* attention-stub latency, >= 1                      */
+  int64_t jitter_us;          /* largest extra latency of a fragment, >= 0         */
+  int64_t cost_fixed_us;      /* step cost per non-empty expert, >= 0              */
+  int64_t cost_row_ns;        /* step cost per row, >= 0                           */
+  int64_t horizon_us;         /* no step starts at or after this time              */
+  uint64_t seed;
+  const int64_t* arrival_us;  /* [n_requests], non-decreasing, >= 0                */
+  const int32_t* out_len;     /* [n_requests], tokens per request, 1..2^20 - 1     */
+  const int64_t* expert_cdf;  /* [n_experts], non-decreasing, last entry > 0       */
+} aep_sim_config;
+
+/* Optional per-step trace (arrays of `capacity` entries; steps beyond it are
+ * counted in the summary but not recorded) and per-request completion times
+ * (done_us [n_requests], -1 if not completed; may be NULL). */
+typedef struct {
+  int64_t capacity;
+  int64_t* t_start;            /* step start (us)                                 */
+  int32_t* block;              /* block run                                       */
+  int32_t* expert;             /* expert run, -1 when a whole block ran           */
+  int64_t* rows;               /* rows drained                                    */
+  int64_t* queued_after;       /* rows left in every queue after the drain        */
+  int32_t* blocks_busy_after;  /* blocks holding any row after the drain          */
+  int64_t* done_us;
+} aep_sim_trace;
+
+typedef struct {
+  int64_t steps;              /* expert steps run                                 */
+  int64_t rows;               /* rows drained in total                            */
+  int64_t busy_us;            /* sum of step durations                            */
+  int64_t end_us;             /* time when the run stopped                        */
+  int64_t token_passes;       /* (token, block) passes completed                  */
+  int64_t requests_done;      /* requests that produced out_len tokens            */
+  int64_t rows_queued_at_end; /* rows still queued when the run stopped           */
+  int64_t recorded;           /* trace entries written                            */
+} aep_sim_summary;
+
+/* Run the model until no step can start (nothing queued and no arrival
+ * pending, or the horizon reached).  trace may be NULL.  AEP_ERR_INVALID_ARG
+ * on a bad config. */
+aep_status aep_sim_run(const aep_sim_config* cfg, aep_sim_trace* trace, aep_sim_summary* out);
+
 /* Executor, re-batch (Sec. 3.2): drain every queue of `layer` into one
  * contiguous batch -- per-expert counts and offsets, then a gather of every
  * queued row into x_perm (a bit copy) -- and empty the layer's queues.  Fills

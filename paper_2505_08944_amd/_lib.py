@@ -45,6 +45,26 @@ class Batch(ctypes.Structure):
                 ("token_weight", ctypes.c_void_p)]
 
 
+class SimConfig(ctypes.Structure):
+    _fields_ = [("n_blocks", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("n_frag", ctypes.c_int32), ("granularity", ctypes.c_int32), ("policy", ctypes.c_int32),
+                ("delta", ctypes.c_double), ("lookahead", ctypes.c_int32), ("n_requests", ctypes.c_int32),
+                ("attn_us", ctypes.c_int64), ("jitter_us", ctypes.c_int64), ("cost_fixed_us", ctypes.c_int64),
+                ("cost_row_ns", ctypes.c_int64), ("horizon_us", ctypes.c_int64), ("seed", ctypes.c_uint64),
+                ("arrival_us", ctypes.c_void_p), ("out_len", ctypes.c_void_p), ("expert_cdf", ctypes.c_void_p)]
+
+
+class SimTrace(ctypes.Structure):
+    _fields_ = [("capacity", ctypes.c_int64), ("t_start", ctypes.c_void_p), ("block", ctypes.c_void_p),
+                ("expert", ctypes.c_void_p), ("rows", ctypes.c_void_p), ("queued_after", ctypes.c_void_p),
+                ("blocks_busy_after", ctypes.c_void_p), ("done_us", ctypes.c_void_p)]
+
+
+class SimSummary(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("steps", "rows", "busy_us", "end_us", "token_passes",
+                                              "requests_done", "rows_queued_at_end", "recorded")]
+
+
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
 _I64 = ctypes.c_int64
@@ -68,6 +88,10 @@ _SIG = {
     "aep_release_batch": (ctypes.c_int, [_P, ctypes.POINTER(Batch)]),
     "aep_sync": (ctypes.c_int, [_P, _P]),
     "aep_fp8_e4m3_to_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "aep_sched_pick": (ctypes.c_int, [_P, _I32, _I32, _I32, ctypes.c_double, _I32, ctypes.POINTER(_I32),
+                                      ctypes.POINTER(_I32)]),
+    "aep_sim_run": (ctypes.c_int, [ctypes.POINTER(SimConfig), ctypes.POINTER(SimTrace),
+                                   ctypes.POINTER(SimSummary)]),
 }
 
 _lib = None
