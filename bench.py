@@ -48,6 +48,9 @@ def parse():
                     help="skip the cold-expert (weight-streaming) measurements")
     ap.add_argument("--sweep", action="store_true",
                     help="also sweep rows per expert (16..256) on same-shape expert groups of >= 1 GB")
+    ap.add_argument("--sched-sim", action="store_true",
+                    help="only run the host expert-runtime model (scheduling policies under a synthetic "
+                         "request stream) and print its JSON summary")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES three times (reference "
                          "kernel for scaling HBM byte counters) and exit")
@@ -89,6 +92,51 @@ def traffic_record(workload: str):
         return None
 
 
+SCHED_POLICIES = [("mtfs", 0.0, 0), ("flfs", 0.0, 0), ("defrag", 0.5, 2), ("defrag", 0.9, 4)]
+
+
+def sched_sim(scenarios=("frag", "livelock"), granularities=("block", "expert"), horizon_us=None):
+    """Scheduling policies on the host expert-runtime model (libaep's
+    aep_sim_run): batch size per step, fragmentation (blocks holding queued
+    rows after a step), decode throughput and request latency."""
+    import synth
+    from paper_2505_08944_amd import sched
+    out = {}
+    for name in scenarios:
+        sc = synth.scenario(name)
+        if horizon_us:
+            sc = __import__("dataclasses").replace(sc, horizon_us=horizon_us)
+        st = synth.request_stream(sc)
+        arr, ol = st["arrival_us"], st["out_len"]
+        res = {"description": sc.description, "requests": int(arr.size), "horizon_s": sc.horizon_us / 1e6}
+        for gran in granularities:
+            for pol, delta, la in SCHED_POLICIES:
+                t0 = time.perf_counter()
+                r = sched.sim_run(n_blocks=sc.n_blocks, n_experts=sc.n_experts, top_k=sc.top_k, n_frag=sc.n_frag,
+                                  granularity=gran, policy=pol, arrival_us=arr, out_len=ol,
+                                  expert_cdf=st["expert_cdf"], attn_us=sc.attn_us, jitter_us=sc.jitter_us,
+                                  cost_fixed_us=sc.cost_fixed_us, cost_row_ns=sc.cost_row_ns,
+                                  horizon_us=sc.horizon_us, seed=sc.cfg_id, delta=delta, lookahead=la,
+                                  trace_capacity=2_000_000)
+                wall = time.perf_counter() - t0
+                done = r["done_us"] >= 0
+                lat = (r["done_us"][done] - arr[done]) / 1e3
+                first_half = arr < sc.horizon_us // 2
+                tr = r["trace"]
+                key = f"{gran}/{pol}" + (f"(d={delta},L={la})" if pol == "defrag" else "")
+                res[key] = {
+                    "steps": r["steps"], "rows_per_step": round(r["rows"] / max(r["steps"], 1), 2),
+                    "blocks_holding_rows": round(float(tr["blocks_busy_after"].mean()), 2) if r["recorded"] else 0.0,
+                    "busy_frac": round(r["busy_us"] / sc.horizon_us, 3),
+                    "decode_tokens_per_s": round(float(ol[done].sum()) / (sc.horizon_us / 1e6), 1),
+                    "requests_done_first_half": round(float(done[first_half].mean()), 4) if first_half.any() else None,
+                    "latency_ms_p50": round(float(np.median(lat)), 1) if lat.size else None,
+                    "latency_ms_p99": round(float(np.percentile(lat, 99)), 1) if lat.size else None,
+                    "rows_queued_at_end": r["rows_queued_at_end"], "model_wall_s": round(wall, 2)}
+        out[name] = res
+    return out
+
+
 def copy_calibration(nbytes: int) -> None:
     import torch
     src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
@@ -103,6 +151,9 @@ def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.sched_sim:
+        print(json.dumps({"sched_sim": sched_sim()}), flush=True)
         return
     if args.gpus != 1:
         sys.stderr.write("bench.py measures one GPU: this build has no multi-GPU path (expert-parallel "

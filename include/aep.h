@@ -223,8 +223,9 @@ typedef struct {
 } aep_sim_config;
 
 /* Optional per-step trace (arrays of `capacity` entries; steps beyond it are
- * counted in the summary but not recorded) and per-request completion times
- * (done_us [n_requests], -1 if not completed; may be NULL). */
+ * counted in the summary but not recorded; block_rows_after may be NULL) and
+ * per-request completion times (done_us [n_requests], -1 if not completed;
+ * may be NULL). */
 typedef struct {
   int64_t capacity;
   int64_t* t_start;            /* step start (us)                                 */
@@ -233,6 +234,8 @@ typedef struct {
   int64_t* rows;               /* rows drained                                    */
   int64_t* queued_after;       /* rows left in every queue after the drain        */
   int32_t* blocks_busy_after;  /* blocks holding any row after the drain          */
+  int64_t* block_rows_after;   /* [capacity][n_blocks] rows queued per block after
+                                  the drain (the queue-depth trace); may be NULL  */
   int64_t* done_us;
 } aep_sim_trace;
 

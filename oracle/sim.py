@@ -132,7 +132,8 @@ def simulate(*, n_blocks: int, n_experts: int, top_k: int, n_frag: int, granular
     t = 0
     steps = rows_total = busy = passes = done = 0
     done_us = [-1] * len(arrival_us)
-    trace = {k: [] for k in ("t_start", "block", "expert", "rows", "queued_after", "blocks_busy_after")}
+    trace = {k: [] for k in ("t_start", "block", "expert", "rows", "queued_after", "blocks_busy_after",
+                             "block_rows_after")}
     while True:
         while heap and heap[0][0] <= t:
             _, _, b, tokens = heapq.heappop(heap)
@@ -189,6 +190,7 @@ def simulate(*, n_blocks: int, n_experts: int, top_k: int, n_frag: int, granular
             trace["rows"].append(rows)
             trace["queued_after"].append(sum(after))
             trace["blocks_busy_after"].append(sum(1 for a in after if a > 0))
+            trace["block_rows_after"].append(after)
             steps += 1
             rows_total += rows
             busy += dur

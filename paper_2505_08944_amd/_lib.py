@@ -57,7 +57,8 @@ class SimConfig(ctypes.Structure):
 class SimTrace(ctypes.Structure):
     _fields_ = [("capacity", ctypes.c_int64), ("t_start", ctypes.c_void_p), ("block", ctypes.c_void_p),
                 ("expert", ctypes.c_void_p), ("rows", ctypes.c_void_p), ("queued_after", ctypes.c_void_p),
-                ("blocks_busy_after", ctypes.c_void_p), ("done_us", ctypes.c_void_p)]
+                ("blocks_busy_after", ctypes.c_void_p), ("block_rows_after", ctypes.c_void_p),
+                ("done_us", ctypes.c_void_p)]
 
 
 class SimSummary(ctypes.Structure):

@@ -305,6 +305,12 @@ aep_status aep_sim_run(const aep_sim_config* cfg, aep_sim_trace* trace, aep_sim_
         trace->rows[recorded] = rows;
         trace->queued_after[recorded] = qa;
         trace->blocks_busy_after[recorded] = busy_blocks;
+        if (trace->block_rows_after)
+          for (int b = 0; b < NB; ++b) {
+            int64_t rb = 0;
+            for (int e = 0; e < NE; ++e) rb += queued(b, e);
+            trace->block_rows_after[recorded * NB + b] = rb;
+          }
         ++recorded;
       }
       ++steps;

@@ -49,10 +49,11 @@ def sim_run(*, n_blocks: int, n_experts: int, top_k: int, n_frag: int, granulari
     cap = int(trace_capacity)
     tr = {"t_start": np.zeros(cap, np.int64), "block": np.zeros(cap, np.int32), "expert": np.zeros(cap, np.int32),
           "rows": np.zeros(cap, np.int64), "queued_after": np.zeros(cap, np.int64),
-          "blocks_busy_after": np.zeros(cap, np.int32)}
+          "blocks_busy_after": np.zeros(cap, np.int32), "block_rows_after": np.zeros((cap, n_blocks), np.int64)}
     done = np.zeros(arr.size, np.int64)
     trace = L.SimTrace(cap, *(tr[k].ctypes.data for k in ("t_start", "block", "expert", "rows", "queued_after",
-                                                          "blocks_busy_after")), done.ctypes.data)
+                                                          "blocks_busy_after", "block_rows_after")),
+                       done.ctypes.data)
     summ = L.SimSummary()
     L.check(L.lib().aep_sim_run(ctypes.byref(cfg), ctypes.byref(trace), ctypes.byref(summ)), "aep_sim_run")
     out: Dict[str, object] = {n: int(getattr(summ, n)) for n, _ in L.SimSummary._fields_}

@@ -8,3 +8,4 @@ from it without sharing any of the method.
 """
 
 from .workloads import *  # noqa: F401,F403
+from .arrivals import *  # noqa: F401,F403
