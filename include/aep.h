@@ -72,6 +72,10 @@ typedef struct {
   int32_t w_dtype;     /* aep_dtype of weights: F32 (with F32 act), BF16 or      */
                        /* FP8_E4M3 (with BF16 act)                               */
   int32_t max_tokens_per_layer; /* queue capacity: tokens a layer may hold     */
+  int32_t token_pool;  /* 1: per-layer token pools for drains of single experts */
+                       /* (aep_route_enqueue_ids ... aep_pool_release); adds    */
+                       /* n_layers * max_tokens_per_layer * (4 d + 8) bytes of  */
+                       /* workspace.  0: none.                                  */
 } aep_config;
 
 /* A drained layer.  Filled by aep_rebatch; all pointers are device views into
@@ -281,6 +285,51 @@ aep_status aep_expert_down(void* ctx, const aep_batch* batch, void* y, void* str
  * y[n_routed + s*n_tokens + t], accumulated in f32 and rounded once.
  * out: device [n_tokens][d] act dtype, caller-owned. */
 aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* out, void* stream);
+
+/* ---- Token pool: top-K merge across drains (Sec. 3.2, top-K support) ----
+ * With single-expert drains a token's k rows run in different drains; its
+ * outputs are merged in a per-layer pool keyed by a caller-chosen token id
+ * (the request slot: the paper keys tokens by request and layer) and the
+ * token is released when all k rows have been merged.  Requires
+ * cfg.token_pool = 1 and n_shared = 0 (else AEP_ERR_UNSUPPORTED).  A layer
+ * fed by aep_route_enqueue_ids is in pool mode until its queues are empty:
+ * aep_route_enqueue, aep_enqueue_rows and aep_rebatch on it return
+ * AEP_ERR_STATE, and aep_route_enqueue_ids on a layer holding rows of
+ * aep_route_enqueue returns AEP_ERR_STATE.  Host-side totals of a pool-mode
+ * layer (aep_queue_depth, aep_pick_layer) are upper bounds. */
+
+/* As aep_route_enqueue, but token t of the fragment gets the caller's id
+ * token_ids[t] (device int32 [T], each in [0, max_tokens_per_layer)) and
+ * claims pool entry (layer, id) for its k rows.  An id whose entry is still
+ * claimed (not yet released), or out of range, sets the device error flag
+ * (reported by aep_sync).  Capacity: every expert queue of the layer must have
+ * room for T more rows (AEP_ERR_CAPACITY otherwise, nothing launched). */
+aep_status aep_route_enqueue_ids(void* ctx, int32_t layer, const void* x, const float* logits,
+                                 int32_t T, const int32_t* token_ids, int32_t* idx_out, float* w_out,
+                                 void* stream);
+
+/* Drain the queue of one expert of a pool-mode layer into a batch whose only
+ * non-empty group is `expert` (counts/offsets of every other group are 0).
+ * The exact row count is on the device (counts[expert]); n_routed = n_rows is
+ * an upper bound known to the host (size y by it), n_tokens = 0 and
+ * token_pos/token_weight are not filled.  Run the FFN as usual, then merge
+ * with aep_pool_accumulate (aep_combine refuses such a batch).
+ * AEP_ERR_EMPTY when the expert's queue is known to be empty, AEP_ERR_STATE as
+ * for aep_rebatch. */
+aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batch* out, void* stream);
+
+/* pool[layer][row_token[r]] += row_weight[r] * y[r] (f32 fused multiply-add)
+ * for every row r of a single-expert batch, and one more of that token's k
+ * rows is merged.  y: device [n_rows][d] act dtype. */
+aep_status aep_pool_accumulate(void* ctx, const aep_batch* batch, const void* y, void* stream);
+
+/* Release every token of `layer` whose k rows have all been merged:
+ * out[id] = the pool sum rounded once to the act dtype, the pool entry is
+ * cleared and the id may be enqueued again; ready[id] = 1 for a released
+ * token, 0 otherwise.  out: device [max_tokens_per_layer][d] act dtype (rows of
+ * tokens not released are left untouched); ready: device int32
+ * [max_tokens_per_layer] or NULL. */
+aep_status aep_pool_release(void* ctx, int32_t layer, void* out, int32_t* ready, void* stream);
 
 /* Release a batch; its buffers may then be reused by the next aep_rebatch. */
 aep_status aep_release_batch(void* ctx, aep_batch* batch);

@@ -34,7 +34,7 @@ class Config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("n_shared", ctypes.c_int32),
                 ("d_model", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("renorm", ctypes.c_int32), ("act_dtype", ctypes.c_int32), ("w_dtype", ctypes.c_int32),
-                ("max_tokens_per_layer", ctypes.c_int32)]
+                ("max_tokens_per_layer", ctypes.c_int32), ("token_pool", ctypes.c_int32)]
 
 
 class Batch(ctypes.Structure):
@@ -89,6 +89,10 @@ _SIG = {
     "aep_release_batch": (ctypes.c_int, [_P, ctypes.POINTER(Batch)]),
     "aep_sync": (ctypes.c_int, [_P, _P]),
     "aep_fp8_e4m3_to_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "aep_route_enqueue_ids": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _P, _P, _P, _P]),
+    "aep_rebatch_expert": (ctypes.c_int, [_P, _I32, _I32, ctypes.POINTER(Batch), _P]),
+    "aep_pool_accumulate": (ctypes.c_int, [_P, ctypes.POINTER(Batch), _P, _P]),
+    "aep_pool_release": (ctypes.c_int, [_P, _I32, _P, _P, _P]),
     "aep_sched_pick": (ctypes.c_int, [_P, _I32, _I32, _I32, ctypes.c_double, _I32, ctypes.POINTER(_I32),
                                       ctypes.POINTER(_I32)]),
     "aep_sim_run": (ctypes.c_int, [ctypes.POINTER(SimConfig), ctypes.POINTER(SimTrace),

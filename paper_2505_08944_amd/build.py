@@ -22,7 +22,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libaep.so")
 
-SOURCES = ["api.hip", "k_route.hip", "k_rebatch.hip", "k_ffn.hip", "k_combine.hip", "sched.hip"]
+SOURCES = ["api.hip", "k_route.hip", "k_rebatch.hip", "k_ffn.hip", "k_combine.hip", "k_pool.hip", "sched.hip"]
 ARCH = "gfx950"
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

@@ -87,7 +87,7 @@ class Context:
 
     def __init__(self, n_layers: int, n_experts: int, d_model: int, d_ffn: int, top_k: int, *,
                  n_shared: int = 0, renorm: bool = True, act: str = "bf16", wdt: str = "bf16",
-                 max_tokens_per_layer: int, device: Optional[torch.device] = None):
+                 max_tokens_per_layer: int, token_pool: bool = False, device: Optional[torch.device] = None):
         self.lib = L.lib()
         self.n_layers, self.n_experts, self.n_shared = n_layers, n_experts, n_shared
         self.d_model, self.d_ffn, self.top_k = d_model, d_ffn, top_k
@@ -95,7 +95,8 @@ class Context:
         self.act, self.wdt = act, wdt
         act_code, self.act_torch = _ACT[act]
         cfg = L.Config(n_layers, n_experts, n_shared, d_model, d_ffn, top_k, int(bool(renorm)), act_code,
-                       _WDT[wdt], max_tokens_per_layer)
+                       _WDT[wdt], max_tokens_per_layer, int(bool(token_pool)))
+        self.max_tokens = max_tokens_per_layer
         h = ctypes.c_void_p()
         L.check(self.lib.aep_create(ctypes.byref(cfg), ctypes.byref(h)), "aep_create")
         self.h = h
@@ -156,6 +157,24 @@ class Context:
             self._frag_refs[layer].append(logits)
         return (idx, w) if routing_out else None
 
+    def route_enqueue_ids(self, layer: int, x: torch.Tensor, logits: torch.Tensor, token_ids: torch.Tensor,
+                          routing_out: bool = False) -> Optional[Tuple[torch.Tensor, torch.Tensor]]:
+        """Route a fragment whose tokens carry caller ids (token-pool mode)."""
+        T = x.shape[0]
+        _need(x, "x", self.act_torch, (T, self.d_model))
+        _need(logits, "logits", torch.float32, (T, self.n_experts))
+        _need(token_ids, "token_ids", torch.int32, (T,))
+        idx = w = None
+        if routing_out:
+            idx = torch.empty((T, self.top_k), dtype=torch.int32, device=x.device)
+            w = torch.empty((T, self.top_k), dtype=torch.float32, device=x.device)
+        L.check(self.lib.aep_route_enqueue_ids(self.h, layer, x.data_ptr(), logits.data_ptr(), T,
+                                               token_ids.data_ptr(), _ptr(idx), _ptr(w), _stream()),
+                "aep_route_enqueue_ids")
+        if T:
+            self._frag_refs[layer].extend([x, logits, token_ids])
+        return (idx, w) if routing_out else None
+
     def enqueue_rows(self, layer: int, expert: int, rows: torch.Tensor, token_ids: torch.Tensor,
                      gate_w: torch.Tensor, n_tokens: int, slots: Optional[torch.Tensor] = None) -> None:
         n = rows.shape[0]
@@ -197,6 +216,30 @@ class Context:
         bv._frags = self._frag_refs[layer]   # rows stay referenced until the batch is released
         self._frag_refs[layer] = []
         return bv
+
+    def rebatch_expert(self, layer: int, expert: int) -> BatchView:
+        """Drain one expert's queue of a token-pool layer."""
+        b = L.Batch()
+        L.check(self.lib.aep_rebatch_expert(self.h, layer, expert, ctypes.byref(b), _stream()),
+                "aep_rebatch_expert")
+        bv = BatchView(self, b)
+        if self.queue_depth(layer)[1] == 0:   # the last queued row of these fragments is in this batch
+            bv._frags = self._frag_refs[layer]
+            self._frag_refs[layer] = []
+        return bv
+
+    def pool_accumulate(self, batch: BatchView, y: torch.Tensor) -> None:
+        _need(y, "y", self.act_torch, (batch.n_rows, self.d_model))
+        L.check(self.lib.aep_pool_accumulate(self.h, ctypes.byref(batch.c), y.data_ptr(), _stream()),
+                "aep_pool_accumulate")
+
+    def pool_release(self, layer: int, out: torch.Tensor, ready: Optional[torch.Tensor] = None) -> None:
+        """Write every completed token of the layer's pool to out[id]; ready[id] = 1 for those."""
+        _need(out, "out", self.act_torch, (self.max_tokens, self.d_model))
+        if ready is not None:
+            _need(ready, "ready", torch.int32, (self.max_tokens,))
+        L.check(self.lib.aep_pool_release(self.h, layer, out.data_ptr(), _ptr(ready), _stream()),
+                "aep_pool_release")
 
     def expert_ffn(self, batch: BatchView, y: Optional[torch.Tensor] = None) -> torch.Tensor:
         if y is None:

@@ -74,11 +74,14 @@ constexpr int kBN32 = 64;
 hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,
                         float* r_w, int32_t* r_rank, int32_t* blockcnt, int32_t* idx_out,
                         float* w_out, int32_t* err, hipStream_t s);
+// token_ids == nullptr: token t of the fragment is token_base + t.  Else its
+// id is token_ids[t] (< n_ids) and it claims pool entry live[id] / pend[id].
 hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* r_rank,
                          const int32_t* blockcnt, int T, int E, int k, const char* x,
                          int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
                          int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
-                         hipStream_t s);
+                         const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
+                         int32_t* err, hipStream_t s);
 hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_t* token_ids,
                                const int32_t* slots, const float* gate_w, int n, int n_tokens,
                                int k, int expert, int E, const int32_t* depth_cur,
@@ -87,13 +90,25 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
 // tile_totals[4]: gate/up big, gate/up small, down big, down small.  nt[4]:
 // column tiles per row tile in the same order.  small_bm = 0 disables the
 // small family (every row in big tiles of big_bm).
-hipError_t launch_plan(int E, int S, int n_tokens, int k, int32_t* depth, int32_t* counts,
-                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, const int* nt,
-                       int big_bm, int small_bm, int32_t* pos, float* posw, hipStream_t s);
+// only_expert >= 0: drain that expert's queue alone (every other group gets
+// 0 rows and keeps its queue).
+hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
+                       int32_t* counts, int32_t* offsets, GroupDesc* groups, int32_t* tile_totals,
+                       const int* nt, int big_bm, int small_bm, int32_t* pos, float* posw,
+                       hipStream_t s);
+// N bounds the routed rows (the exact count is offsets[E] on the device);
+// pos == nullptr skips the (token, slot) -> row map.
 hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,
                          int64_t N, int n_tokens, int shared, const void* const* tok_row,
                          char* xp, int64_t row_bytes, int32_t* row_token, float* row_w,
                          int32_t* pos, float* posw, int k, int32_t* err, hipStream_t s);
+// token pool: rows [0, offsets[E]) of a batch (N bounds them) are merged into
+// pool[row_token[r]]; release writes out / ready for completed ids.
+hipError_t launch_pool_accumulate(int act_dtype, const void* y, int64_t N, const int32_t* offsets,
+                                  int E, const int32_t* row_token, const float* row_w, float* pool,
+                                  int32_t* pend, int d, hipStream_t s);
+hipError_t launch_pool_release(int act_dtype, float* pool, int32_t* live, int32_t* pend, int n_ids,
+                               void* out, int32_t* ready, int d, hipStream_t s);
 // stage 0: gate/up (xp -> h), stage 1: down (h -> y); max_tiles bounds the
 // stage's tile count (the exact count is on the device).
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,

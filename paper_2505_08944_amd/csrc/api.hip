@@ -19,12 +19,19 @@ using namespace aep;
 namespace {
 
 struct LayerState {
-  int32_t tokens = 0;         // layer-local token ids handed out / declared
-  int64_t rows = 0;           // queued rows
-  int64_t routed_tokens = 0;  // tokens that came through the router
-  std::vector<int64_t> explicit_rows;  // per expert, rows from aep_enqueue_rows
-  int cur = 0;                         // current half of the depth ping-pong
-  std::vector<uint8_t> have_w;         // weights registered, per group
+  int32_t tokens = 0;          // layer-local token ids handed out / declared
+  int64_t rows = 0;            // queued rows (an upper bound in pool mode)
+  std::vector<int64_t> bound;  // per expert, an upper bound of its queue depth
+  bool pool = false;           // fed by aep_route_enqueue_ids (token-pool mode)
+  int cur = 0;                 // current half of the depth ping-pong
+  std::vector<uint8_t> have_w; // weights registered, per group
+
+  void clear() {
+    tokens = 0;
+    rows = 0;
+    pool = false;
+    std::fill(bound.begin(), bound.end(), 0);
+  }
 };
 
 struct Ctx {
@@ -36,6 +43,7 @@ struct Ctx {
   size_t off_ridx = 0, off_rw = 0, off_rrank = 0, off_blockcnt = 0;
   size_t off_counts = 0, off_offsets = 0, off_groups = 0, off_tiles = 0;
   size_t off_xp = 0, off_rowtok = 0, off_roww = 0, off_pos = 0, off_posw = 0, off_h = 0;
+  size_t off_pool = 0, off_live = 0, off_pend = 0;  // token pools (cfg.token_pool)
   size_t ws_need = 0;
   char* ws = nullptr;
   int device = -1;
@@ -43,6 +51,7 @@ struct Ctx {
   std::vector<LayerState> layers;
   std::vector<WeightDesc> wtab_host;  // [layer][group]
   bool batch_out = false;
+  bool batch_expert = false;  // the outstanding batch is a single-expert drain
   uint64_t epoch = 0;
   int32_t batch_layer = -1;
 
@@ -61,6 +70,11 @@ struct Ctx {
   WeightDesc* wtab(int layer) const {
     return reinterpret_cast<WeightDesc*>(ws + off_wtab) + (int64_t)layer * G;
   }
+  float* pool(int layer) const {
+    return reinterpret_cast<float*>(ws + off_pool) + (int64_t)layer * tmax() * cfg.d_model;
+  }
+  int32_t* live(int layer) const { return reinterpret_cast<int32_t*>(ws + off_live) + (int64_t)layer * tmax(); }
+  int32_t* pend(int layer) const { return reinterpret_cast<int32_t*>(ws + off_pend) + (int64_t)layer * tmax(); }
   template <typename T>
   T* at(size_t off) const {
     return reinterpret_cast<T*>(ws + off);
@@ -101,6 +115,11 @@ bool layout(Ctx& c) {
   c.off_pos = take(sizeof(int32_t) * N);
   c.off_posw = take(sizeof(float) * N);
   c.off_h = take((size_t)hrows * f * c.esz);
+  if (g.token_pool) {
+    c.off_pool = take(sizeof(float) * L * T * d);
+    c.off_live = take(sizeof(int32_t) * L * T);
+    c.off_pend = take(sizeof(int32_t) * L * T);
+  }
   c.ws_need = o;
   return true;
 }
@@ -160,6 +179,8 @@ aep_status aep_create(const aep_config* cfg, void** out) {
   if (g.top_k < 1 || g.top_k > g.n_experts || g.top_k > kMaxTopK) return AEP_ERR_INVALID_ARG;
   if (g.renorm != 0 && g.renorm != 1) return AEP_ERR_INVALID_ARG;
   if (g.max_tokens_per_layer < 1 || g.max_tokens_per_layer > kTokenMask) return AEP_ERR_INVALID_ARG;
+  if (g.token_pool != 0 && g.token_pool != 1) return AEP_ERR_INVALID_ARG;
+  if (g.token_pool && g.n_shared > 0) return AEP_ERR_UNSUPPORTED;
   const bool f32 = g.act_dtype == AEP_F32 && g.w_dtype == AEP_F32;
   const bool bf = g.act_dtype == AEP_BF16 && (g.w_dtype == AEP_BF16 || g.w_dtype == AEP_FP8_E4M3);
   if (!f32 && !bf) {
@@ -174,7 +195,7 @@ aep_status aep_create(const aep_config* cfg, void** out) {
   layout(*c);
   c->layers.resize(g.n_layers);
   for (auto& l : c->layers) {
-    l.explicit_rows.assign(g.n_experts, 0);
+    l.bound.assign(g.n_experts, 0);
     l.have_w.assign(c->G, 0);
   }
   c->wtab_host.assign((size_t)g.n_layers * c->G, WeightDesc{});
@@ -209,18 +230,19 @@ aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream)
   if (hipMemsetAsync(ws + c->off_err, 0, c->off_q - c->off_err, s) != hipSuccess) return AEP_ERR_DEVICE;
   if (hipMemsetAsync(ws + c->off_wtab, 0, sizeof(WeightDesc) * c->cfg.n_layers * c->G, s) != hipSuccess)
     return AEP_ERR_DEVICE;
+  if (c->cfg.token_pool && hipMemsetAsync(ws + c->off_pool, 0, c->ws_need - c->off_pool, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
   if (hipStreamSynchronize(s) != hipSuccess) return AEP_ERR_DEVICE;
   c->ws = ws;
   c->device = devid;
   c->num_cu = ncu > 0 ? ncu : 1;
   for (auto& l : c->layers) {
-    l.tokens = 0;
-    l.rows = 0;
-    l.routed_tokens = 0;
+    l.clear();
     l.cur = 0;
-    std::fill(l.explicit_rows.begin(), l.explicit_rows.end(), 0);
     std::fill(l.have_w.begin(), l.have_w.end(), 0);
   }
+  c->batch_out = false;
+  c->batch_expert = false;
   std::fill(c->wtab_host.begin(), c->wtab_host.end(), WeightDesc{});
   return AEP_OK;
 }
@@ -250,21 +272,23 @@ aep_status aep_set_expert_weights(void* ctx, int32_t layer, int32_t expert, cons
   return AEP_OK;
 }
 
-aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
-                             int32_t* idx_out, float* w_out, void* stream) {
-  Ctx* c = as_ctx(ctx);
+static aep_status route_common(Ctx* c, int32_t layer, const void* x, const float* logits, int32_t T,
+                               const int32_t* token_ids, int32_t* idx_out, float* w_out, void* stream) {
   if (!c) return AEP_ERR_INVALID_ARG;
   if (!c->ws) return AEP_ERR_STATE;
   if (layer < 0 || layer >= c->cfg.n_layers || T < 0) return AEP_ERR_INVALID_ARG;
+  if (token_ids && !c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
+  LayerState& L = c->layers[layer];
+  const bool want_pool = token_ids != nullptr;
+  if (L.rows > 0 && L.pool != want_pool) return AEP_ERR_STATE;
   if (T == 0) return AEP_OK;
   if (!x || !logits) return AEP_ERR_INVALID_ARG;
   const int E = c->cfg.n_experts, k = c->cfg.top_k;
   if (E > kMaxRouteExperts) return AEP_ERR_UNSUPPORTED;
-  LayerState& L = c->layers[layer];
   int64_t ub = 0;
-  for (int e = 0; e < E; ++e) ub = std::max(ub, L.routed_tokens + L.explicit_rows[e]);
-  if ((int64_t)L.tokens + T > c->tmax() || ub + T > c->tmax() || L.rows + (int64_t)T * k > c->row_cap())
-    return AEP_ERR_CAPACITY;
+  for (int e = 0; e < E; ++e) ub = std::max(ub, L.bound[e]);
+  if (ub + T > c->tmax() || L.rows + (int64_t)T * k > c->row_cap()) return AEP_ERR_CAPACITY;
+  if (!want_pool && (int64_t)L.tokens + T > c->tmax()) return AEP_ERR_CAPACITY;
   hipStream_t s = as_stream(stream);
   int32_t* ridx = c->at<int32_t>(c->off_ridx);
   float* rw = c->at<float>(c->off_rw);
@@ -275,14 +299,31 @@ aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const floa
   if (e1 != hipSuccess) return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   hipError_t e2 = launch_append(ridx, rw, rrank, bcnt, T, E, k, reinterpret_cast<const char*>(x), row_bytes,
-                                L.tokens, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), c->q(layer),
-                                c->tmax(), c->tokrow(layer), s);
+                                want_pool ? 0 : L.tokens, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1),
+                                c->q(layer), c->tmax(), c->tokrow(layer), token_ids, (int)c->tmax(),
+                                want_pool ? c->live(layer) : nullptr, want_pool ? c->pend(layer) : nullptr,
+                                c->err(), s);
   if (e2 != hipSuccess) return AEP_ERR_DEVICE;
   L.cur ^= 1;
-  L.tokens += T;
+  if (!want_pool) L.tokens += T;
+  L.pool = want_pool;
   L.rows += (int64_t)T * k;
-  L.routed_tokens += T;
+  for (int e = 0; e < E; ++e) L.bound[e] += T;
   return AEP_OK;
+}
+
+aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
+                             int32_t* idx_out, float* w_out, void* stream) {
+  return route_common(as_ctx(ctx), layer, x, logits, T, nullptr, idx_out, w_out, stream);
+}
+
+aep_status aep_route_enqueue_ids(void* ctx, int32_t layer, const void* x, const float* logits,
+                                 int32_t T, const int32_t* token_ids, int32_t* idx_out, float* w_out,
+                                 void* stream) {
+  if (T > 0 && !token_ids) return AEP_ERR_INVALID_ARG;
+  Ctx* c = as_ctx(ctx);
+  if (c && T == 0 && !c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
+  return route_common(c, layer, x, logits, T, T > 0 ? token_ids : nullptr, idx_out, w_out, stream);
 }
 
 aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void* rows,
@@ -294,11 +335,11 @@ aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void
   if (layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->cfg.n_experts || n < 0)
     return AEP_ERR_INVALID_ARG;
   if (c->cfg.n_shared > 0) return AEP_ERR_UNSUPPORTED;
+  LayerState& L = c->layers[layer];
+  if (L.rows > 0 && L.pool) return AEP_ERR_STATE;
   if (n == 0) return AEP_OK;
   if (!rows || !token_ids || !gate_w || n_tokens < 1) return AEP_ERR_INVALID_ARG;
-  LayerState& L = c->layers[layer];
-  if ((int64_t)n_tokens > c->tmax() || L.routed_tokens + L.explicit_rows[expert] + n > c->tmax() ||
-      L.rows + n > c->row_cap())
+  if ((int64_t)n_tokens > c->tmax() || L.bound[expert] + n > c->tmax() || L.rows + n > c->row_cap())
     return AEP_ERR_CAPACITY;
   hipStream_t s = as_stream(stream);
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
@@ -308,9 +349,10 @@ aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void
                                      c->tmax(), c->err(), s);
   if (e != hipSuccess) return AEP_ERR_DEVICE;
   L.cur ^= 1;
+  L.pool = false;
   L.tokens = std::max(L.tokens, n_tokens);
   L.rows += n;
-  L.explicit_rows[expert] += n;
+  L.bound[expert] += n;
   return AEP_OK;
 }
 
@@ -386,6 +428,7 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   if (!c || !out || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
   if (!c->ws || c->batch_out) return AEP_ERR_STATE;
   LayerState& L = c->layers[layer];
+  if (L.rows > 0 && L.pool) return AEP_ERR_STATE;  // pool-mode layers drain one expert at a time
   if (L.rows == 0 && !(c->cfg.n_shared > 0 && L.tokens > 0)) return AEP_ERR_EMPTY;
   for (int g = 0; g < c->G; ++g)
     if (!L.have_w[g]) return AEP_ERR_STATE;
@@ -397,8 +440,9 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   int32_t* offsets = c->at<int32_t>(c->off_offsets);
   int32_t* pos = c->at<int32_t>(c->off_pos);
   float* posw = c->at<float>(c->off_posw);
-  if (launch_plan(E, S, L.tokens, k, c->depth(layer, L.cur), counts, offsets, c->at<GroupDesc>(c->off_groups),
-                  c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, pos, posw, s) != hipSuccess)
+  if (launch_plan(E, S, L.tokens, k, -1, c->depth(layer, L.cur), counts, offsets,
+                  c->at<GroupDesc>(c->off_groups), c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, pos,
+                  posw, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, L.rows, L.tokens, S > 0, c->tokrow(layer),
@@ -407,6 +451,7 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
     return AEP_ERR_DEVICE;
   c->epoch += 1;
   c->batch_out = true;
+  c->batch_expert = false;
   c->batch_layer = layer;
   out->layer = layer;
   out->n_tokens = L.tokens;
@@ -420,10 +465,56 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   out->row_weight = c->at<float>(c->off_roww);
   out->token_pos = pos;
   out->token_weight = posw;
-  L.tokens = 0;
-  L.rows = 0;
-  L.routed_tokens = 0;
-  std::fill(L.explicit_rows.begin(), L.explicit_rows.end(), 0);
+  L.clear();
+  return AEP_OK;
+}
+
+aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batch* out, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !out || layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->cfg.n_experts)
+    return AEP_ERR_INVALID_ARG;
+  if (!c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
+  if (!c->ws || c->batch_out) return AEP_ERR_STATE;
+  LayerState& L = c->layers[layer];
+  if (L.rows > 0 && !L.pool) return AEP_ERR_STATE;
+  const int64_t nb = std::min(L.bound[expert], L.rows);
+  if (nb == 0) return AEP_ERR_EMPTY;
+  if (!L.have_w[expert]) return AEP_ERR_STATE;
+  int nt[4], big_bm, small_bm;
+  tiling(*c, nt, &big_bm, &small_bm);
+  hipStream_t s = as_stream(stream);
+  const int E = c->cfg.n_experts, k = c->cfg.top_k;
+  int32_t* counts = c->at<int32_t>(c->off_counts);
+  int32_t* offsets = c->at<int32_t>(c->off_offsets);
+  if (launch_plan(E, 0, 0, k, expert, c->depth(layer, L.cur), counts, offsets, c->at<GroupDesc>(c->off_groups),
+                  c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, nullptr, nullptr, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
+  if (launch_gather(c->q(layer), c->tmax(), offsets, E, nb, 0, 0, c->tokrow(layer), c->at<char>(c->off_xp),
+                    row_bytes, c->at<int32_t>(c->off_rowtok), c->at<float>(c->off_roww), nullptr, nullptr, k,
+                    c->err(), s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  c->epoch += 1;
+  c->batch_out = true;
+  c->batch_expert = true;
+  c->batch_layer = layer;
+  out->layer = layer;
+  out->n_tokens = 0;
+  out->n_routed = nb;
+  out->n_rows = nb;
+  out->epoch = c->epoch;
+  out->x_perm = c->ws + c->off_xp;
+  out->counts = counts;
+  out->offsets = offsets;
+  out->row_token = c->at<int32_t>(c->off_rowtok);
+  out->row_weight = c->at<float>(c->off_roww);
+  out->token_pos = nullptr;
+  out->token_weight = nullptr;
+  L.bound[expert] = 0;
+  int64_t sum = 0;
+  for (int e = 0; e < E; ++e) sum += L.bound[e];
+  L.rows = std::min(L.rows, sum);
+  if (L.rows == 0) L.clear();
   return AEP_OK;
 }
 
@@ -471,10 +562,32 @@ aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* o
   Ctx* c = as_ctx(ctx);
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
+  if (c->batch_expert) return AEP_ERR_STATE;
   if (!y || !out) return AEP_ERR_INVALID_ARG;
   return dev(launch_combine(c->cfg.act_dtype, y, batch->n_routed, batch->n_tokens, c->cfg.n_shared,
                             c->cfg.top_k, batch->token_pos, batch->token_weight, out, c->cfg.d_model,
                             as_stream(stream)));
+}
+
+aep_status aep_pool_accumulate(void* ctx, const aep_batch* batch, const void* y, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  aep_status st = check_batch(c, batch);
+  if (st != AEP_OK) return st;
+  if (!c->batch_expert) return AEP_ERR_STATE;
+  if (!y) return AEP_ERR_INVALID_ARG;
+  return dev(launch_pool_accumulate(c->cfg.act_dtype, y, batch->n_routed, batch->offsets, c->cfg.n_experts,
+                                    batch->row_token, batch->row_weight, c->pool(batch->layer),
+                                    c->pend(batch->layer), c->cfg.d_model, as_stream(stream)));
+}
+
+aep_status aep_pool_release(void* ctx, int32_t layer, void* out, int32_t* ready, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
+  if (!c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
+  if (!c->ws) return AEP_ERR_STATE;
+  if (!out) return AEP_ERR_INVALID_ARG;
+  return dev(launch_pool_release(c->cfg.act_dtype, c->pool(layer), c->live(layer), c->pend(layer),
+                                 (int)c->tmax(), out, ready, c->cfg.d_model, as_stream(stream)));
 }
 
 aep_status aep_release_batch(void* ctx, aep_batch* batch) {
@@ -482,6 +595,7 @@ aep_status aep_release_batch(void* ctx, aep_batch* batch) {
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
   c->batch_out = false;
+  c->batch_expert = false;
   c->batch_layer = -1;
   std::memset(batch, 0, sizeof(*batch));
   return AEP_OK;

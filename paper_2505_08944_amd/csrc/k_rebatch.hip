@@ -1,9 +1,9 @@
 // Executor re-batch kernels: drain plan + gather.
 //
-// plan (one workgroup): reads the drained layer's per-expert queue depths,
-// writes counts / exclusive-scan offsets / the FFN group table (row bases and
-// tile ranges), resets the queue depths to zero and clears the (token, slot)
-// -> row map.
+// plan (one workgroup): reads the drained layer's per-expert queue depths
+// (or one expert's, for a single-expert drain), writes counts / exclusive-scan
+// offsets / the FFN group table (row bases and tile ranges), resets the
+// drained queue depths to zero and clears the (token, slot) -> row map.
 //
 // gather: one wave per batch row.  A routed row finds its expert by binary
 // search over the offsets, reads its queue entry and copies the referenced
@@ -16,7 +16,7 @@
 namespace aep {
 
 __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, int k,
-                                                    int32_t* __restrict__ depth,
+                                                    int only_expert, int32_t* __restrict__ depth,
                                                     int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ offsets,
                                                     GroupDesc* __restrict__ groups,
@@ -28,7 +28,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
   __shared__ int32_t cnt[kMaxGroups];
   const int tid = threadIdx.x;
   const int G = E + S;
-  for (int g = tid; g < G; g += blockDim.x) cnt[g] = g < E ? depth[g] : n_tokens;
+  for (int g = tid; g < G; g += blockDim.x)
+    cnt[g] = g < E ? (only_expert < 0 || g == only_expert ? depth[g] : 0) : n_tokens;
   __syncthreads();
   if (tid == 0) {
     int N = 0;
@@ -74,7 +75,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
     offsets[G] = off;
     for (int i = 0; i < 4; ++i) tile_totals[i] = t[i];
   }
-  for (int e = tid; e < E; e += blockDim.x) depth[e] = 0;  // the layer's queues are drained
+  for (int e = tid; e < E; e += blockDim.x)  // the drained queues are empty again
+    if (only_expert < 0 || e == only_expert) depth[e] = 0;
   const int64_t nk = (int64_t)n_tokens * k;
   for (int64_t i = tid; i < nk; i += blockDim.x) {
     pos[i] = -1;
@@ -94,6 +96,7 @@ __global__ __launch_bounds__(256) void gather_kernel(
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t R = N + (shared ? n_tokens : 0);
   if (r >= R) return;
+  if (r < N && r >= off_s[E]) return;  // N only bounds the routed rows
   const uint4* src;
   if (r < N) {
     int lo = 0, hi = E;  // off_s[lo] <= r < off_s[hi]
@@ -111,10 +114,12 @@ __global__ __launch_bounds__(256) void gather_kernel(
       const int slot = (int)((uint32_t)en.token_slot >> kTokenBits);
       row_token[r] = tok;
       row_w[r] = en.w;
-      const int64_t pi = (int64_t)tok * k + slot;
-      const int old = atomicExch(&pos[pi], (int)r);
-      posw[pi] = en.w;
-      if (old != -1) atomicOr(err, kErrCollision);
+      if (pos) {
+        const int64_t pi = (int64_t)tok * k + slot;
+        const int old = atomicExch(&pos[pi], (int)r);
+        posw[pi] = en.w;
+        if (old != -1) atomicOr(err, kErrCollision);
+      }
     }
   } else {
     src = reinterpret_cast<const uint4*>(tok_row[r - N]);
@@ -125,11 +130,12 @@ __global__ __launch_bounds__(256) void gather_kernel(
   for (int c = lane; c < nchunk; c += 64) dst[c] = src[c];
 }
 
-hipError_t launch_plan(int E, int S, int n_tokens, int k, int32_t* depth, int32_t* counts,
-                       int32_t* offsets, GroupDesc* groups, int32_t* tile_totals, const int* nt,
-                       int big_bm, int small_bm, int32_t* pos, float* posw, hipStream_t s) {
-  plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, depth, counts, offsets, groups, tile_totals,
-                                  nt[0], nt[1], nt[2], nt[3], big_bm, small_bm, pos, posw);
+hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
+                       int32_t* counts, int32_t* offsets, GroupDesc* groups, int32_t* tile_totals,
+                       const int* nt, int big_bm, int small_bm, int32_t* pos, float* posw,
+                       hipStream_t s) {
+  plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, only_expert, depth, counts, offsets, groups,
+                                  tile_totals, nt[0], nt[1], nt[2], nt[3], big_bm, small_bm, pos, posw);
   return hipGetLastError();
 }
 

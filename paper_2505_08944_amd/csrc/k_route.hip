@@ -133,7 +133,8 @@ __global__ __launch_bounds__(kRouteThreads) void append_kernel(
     const int32_t* __restrict__ r_rank, const int32_t* __restrict__ blockcnt, int T, int E, int k,
     const char* x, int64_t row_bytes, int32_t token_base, const int32_t* __restrict__ depth_cur,
     int32_t* __restrict__ depth_nxt, QEntry* __restrict__ q, int64_t q_stride,
-    const void** __restrict__ tok_row) {
+    const void** __restrict__ tok_row, const int32_t* __restrict__ token_ids, int n_ids,
+    int32_t* __restrict__ live, int32_t* __restrict__ pend, int32_t* __restrict__ err) {
   __shared__ int32_t base[kMaxRouteExperts];
   const int tid = threadIdx.x;
   if (tid < E) {
@@ -146,16 +147,29 @@ __global__ __launch_bounds__(kRouteThreads) void append_kernel(
   const int t = blockIdx.x * kRouteThreads + tid;
   if (t >= T) return;
   const char* row = x + (int64_t)t * row_bytes;
+  int tok = token_base + t;
+  if (token_ids) {
+    // caller id: claim its pool entry (an id still claimed, or out of
+    // range, is an error; the row is filed under a clamped id)
+    tok = token_ids[t];
+    if (tok < 0 || tok >= n_ids) {
+      atomicOr(err, kErrTokenRange);
+      tok = tok < 0 ? 0 : n_ids - 1;
+    } else if (atomicExch(&live[tok], 1) != 0) {
+      atomicOr(err, kErrCollision);
+    }
+    pend[tok] = k;
+  }
   for (int j = 0; j < k; ++j) {
     const int64_t o = (int64_t)t * k + j;
     const int e = r_idx[o];
     QEntry en;
     en.row = row;
-    en.token_slot = (token_base + t) | (j << kTokenBits);
+    en.token_slot = tok | (j << kTokenBits);
     en.w = r_w[o];
     q[(int64_t)e * q_stride + base[e] + r_rank[o]] = en;
   }
-  tok_row[token_base + t] = row;
+  tok_row[tok] = row;
 }
 
 __global__ __launch_bounds__(256) void enqueue_rows_kernel(
@@ -210,10 +224,12 @@ hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* 
                          const int32_t* blockcnt, int T, int E, int k, const char* x,
                          int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
                          int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
-                         hipStream_t s) {
+                         const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
+                         int32_t* err, hipStream_t s) {
   const int nb = (T + kRouteThreads - 1) / kRouteThreads;
   append_kernel<<<nb, kRouteThreads, 0, s>>>(r_idx, r_w, r_rank, blockcnt, T, E, k, x, row_bytes,
-                                              token_base, depth_cur, depth_nxt, q, q_stride, tok_row);
+                                              token_base, depth_cur, depth_nxt, q, q_stride, tok_row,
+                                              token_ids, n_ids, live, pend, err);
   return hipGetLastError();
 }
 
