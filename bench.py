@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--sched-sim", action="store_true",
                     help="only run the host expert-runtime model (scheduling policies under a synthetic "
                          "request stream) and print its JSON summary")
+    ap.add_argument("--pool", action="store_true",
+                    help="only time the workload drained one expert at a time through the token pool "
+                         "(route with caller ids, per-expert re-batch + FFN + pool merge, release) and print "
+                         "its JSON summary")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES three times (reference "
                          "kernel for scaling HBM byte counters) and exit")
@@ -137,6 +141,73 @@ def sched_sim(scenarios=("frag", "livelock"), granularities=("block", "expert"),
     return out
 
 
+def pool_measurement(name: str, steps: int, warmup: int, threads: int):
+    """The workload's layer drained expert by expert through the token pool:
+    route with caller ids, then for every expert re-batch, gate/up, down and
+    pool merge, then one release.  Inputs resident in HBM; HIP events on the
+    launch stream around whole steps."""
+    import torch
+    import synth
+    import paper_2505_08944_amd as aep
+    w = synth.workload(name)
+    if w.S or w.mode != "routed" or w.n_layers != 1:
+        raise SystemExit(f"--pool needs a one-layer routed workload without shared experts ({name} is not)")
+    dev = torch.device("cuda", 0)
+    frags = synth.layer_fragments(w, 0)
+    ws = synth.all_expert_weights(w, 0, threads=threads)
+    act = torch.bfloat16 if w.act == "bf16" else torch.float32
+
+    def dev_t(a, fmt):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev) if fmt == "bf16" else \
+            torch.from_numpy(a).to(dev)
+
+    xs = [dev_t(f["x"], w.act) for f in frags]
+    lgs = [dev_t(f["logits"], "f32") for f in frags]
+    T = sum(x.shape[0] for x in xs)
+    ids, o = [], 0
+    for x in xs:
+        ids.append(torch.arange(o, o + x.shape[0], dtype=torch.int32, device=dev))
+        o += x.shape[0]
+    ctx = aep.Context(1, w.E, w.d, w.f, w.k, act=w.act, wdt=w.wdt, max_tokens_per_layer=T, token_pool=True)
+    wdev = []
+    for e, ex in enumerate(ws):
+        t = [dev_t(ex[k], w.wdt) for k in ("gate", "up", "down")]
+        ctx.set_expert_weights(0, e, *t)
+        wdev.append(t)
+    del ws
+    y = torch.empty((T, w.d), dtype=act, device=dev)
+    out = torch.empty((T, w.d), dtype=act, device=dev)
+    ready = torch.empty(T, dtype=torch.int32, device=dev)
+
+    def step():
+        for x, lg, i in zip(xs, lgs, ids):
+            ctx.route_enqueue_ids(0, x, lg, i)
+        for e in range(w.E):
+            b = ctx.rebatch_expert(0, e)
+            ctx.expert_gate_up(b)
+            ctx.expert_down(b, y)
+            ctx.pool_accumulate(b, y)
+            ctx.release(b)
+        ctx.pool_release(0, out, ready)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ctx.sync()
+    ms = e0.elapsed_time(e1) / steps
+    released = int(ready.sum().item())
+    return {"workload": w.description or w.name, "mode": "expert-by-expert drains through the token pool",
+            "tokens": T, "ms_per_step": round(ms, 4), "tokens_per_s": round(T / ms * 1e3, 1),
+            "released_last_step": released, "steps": steps, "warmup": warmup}
+
+
 def copy_calibration(nbytes: int) -> None:
     import torch
     src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
@@ -154,6 +225,10 @@ def main():
         return
     if args.sched_sim:
         print(json.dumps({"sched_sim": sched_sim()}), flush=True)
+        return
+    if args.pool:
+        print(json.dumps({"pool": pool_measurement(args.workload, args.steps, args.warmup, args.threads)}),
+              flush=True)
         return
     if args.gpus != 1:
         sys.stderr.write("bench.py measures one GPU: this build has no multi-GPU path (expert-parallel "
