@@ -91,11 +91,13 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
 // column tiles per row tile in the same order.  small_bm = 0 disables the
 // small family (every row in big tiles of big_bm).
 // only_expert >= 0: drain that expert's queue alone (every other group gets
-// 0 rows and keeps its queue).
+// 0 rows and keeps its queue).  depth is the current half of the layer's
+// depth ping-pong, depth_other the other one; both are cleared for the
+// drained experts.
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
-                       int32_t* counts, int32_t* offsets, GroupDesc* groups, int32_t* tile_totals,
-                       const int* nt, int big_bm, int small_bm, int32_t* pos, float* posw,
-                       hipStream_t s);
+                       int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
+                       int32_t* tile_totals, const int* nt, int big_bm, int small_bm, int32_t* pos,
+                       float* posw, hipStream_t s);
 // N bounds the routed rows (the exact count is offsets[E] on the device);
 // pos == nullptr skips the (token, slot) -> row map.
 hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,

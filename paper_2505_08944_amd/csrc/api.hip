@@ -440,7 +440,7 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   int32_t* offsets = c->at<int32_t>(c->off_offsets);
   int32_t* pos = c->at<int32_t>(c->off_pos);
   float* posw = c->at<float>(c->off_posw);
-  if (launch_plan(E, S, L.tokens, k, -1, c->depth(layer, L.cur), counts, offsets,
+  if (launch_plan(E, S, L.tokens, k, -1, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
                   c->at<GroupDesc>(c->off_groups), c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, pos,
                   posw, s) != hipSuccess)
     return AEP_ERR_DEVICE;
@@ -486,7 +486,8 @@ aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batc
   const int E = c->cfg.n_experts, k = c->cfg.top_k;
   int32_t* counts = c->at<int32_t>(c->off_counts);
   int32_t* offsets = c->at<int32_t>(c->off_offsets);
-  if (launch_plan(E, 0, 0, k, expert, c->depth(layer, L.cur), counts, offsets, c->at<GroupDesc>(c->off_groups),
+  if (launch_plan(E, 0, 0, k, expert, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
+                  c->at<GroupDesc>(c->off_groups),
                   c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, nullptr, nullptr, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;

@@ -17,6 +17,7 @@ namespace aep {
 
 __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, int k,
                                                     int only_expert, int32_t* __restrict__ depth,
+                                                    int32_t* __restrict__ depth_other,
                                                     int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ offsets,
                                                     GroupDesc* __restrict__ groups,
@@ -75,8 +76,11 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
     offsets[G] = off;
     for (int i = 0; i < 4; ++i) tile_totals[i] = t[i];
   }
-  for (int e = tid; e < E; e += blockDim.x)  // the drained queues are empty again
-    if (only_expert < 0 || e == only_expert) depth[e] = 0;
+  // The drained queues are empty again, in both halves of the depth
+  // ping-pong: whichever half the next append reads starts from zero (so a
+  // captured drain step replays correctly whatever the parity of its appends).
+  for (int e = tid; e < E; e += blockDim.x)
+    if (only_expert < 0 || e == only_expert) depth[e] = depth_other[e] = 0;
   const int64_t nk = (int64_t)n_tokens * k;
   for (int64_t i = tid; i < nk; i += blockDim.x) {
     pos[i] = -1;
@@ -131,10 +135,10 @@ __global__ __launch_bounds__(256) void gather_kernel(
 }
 
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
-                       int32_t* counts, int32_t* offsets, GroupDesc* groups, int32_t* tile_totals,
-                       const int* nt, int big_bm, int small_bm, int32_t* pos, float* posw,
-                       hipStream_t s) {
-  plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, only_expert, depth, counts, offsets, groups,
+                       int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
+                       int32_t* tile_totals, const int* nt, int big_bm, int small_bm, int32_t* pos,
+                       float* posw, hipStream_t s) {
+  plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, only_expert, depth, depth_other, counts, offsets, groups,
                                   tile_totals, nt[0], nt[1], nt[2], nt[3], big_bm, small_bm, pos, posw);
   return hipGetLastError();
 }
