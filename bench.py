@@ -381,11 +381,18 @@ def main():
     print(json.dumps(res), flush=True)
 
 
-def _flush(buf):
-    buf.add_(1)  # 1 GiB read + write: evicts L2 and the 256 MB Infinity Cache
+def _flush(buf, mode="read"):
+    """Evict L2 and the 256 MB Infinity Cache before a cold measurement by
+    streaming a 1 GiB buffer.  "read" only reads it (the caches then hold
+    clean lines); "write" also writes it, leaving dirty lines whose write-back
+    the measured kernels would pay for."""
+    if mode == "write":
+        buf.add_(1)
+    else:
+        buf.max()
 
 
-def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0):
+def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0, flush="read"):
     """Grouped FFN over explicit per-expert rows (counts `groups`), weights of
     the given format drawn on the device; returns (seconds per gate/up + down,
     algorithmic bytes, flops).  Caches are flushed before every repetition."""
@@ -420,12 +427,14 @@ def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0):
         o += n
     b = ctx.rebatch(0)
     y = torch.empty((b.n_rows, d), dtype=torch.bfloat16, device=dev)
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    flush_mode = flush
+    flush_buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     ctx.expert_gate_up(b)
     ctx.expert_down(b, y)
     times = []
     for _ in range(reps):
-        _flush(flush)
+        if flush_mode != "none":
+            _flush(flush_buf, flush_mode)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         ctx.expert_gate_up(b)
@@ -439,7 +448,7 @@ def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0):
     nonempty = sum(1 for n in groups if n)
     byts = nonempty * wbytes + N * 2 * d * 2
     t = float(np.median(times))
-    del ctx, W, rows, flush
+    del ctx, W, rows, flush_buf
     torch.cuda.empty_cache()
     return t, byts, 6.0 * d * f * N
 
