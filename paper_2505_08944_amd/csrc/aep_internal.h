@@ -32,20 +32,23 @@ struct WeightDesc {
 static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 
 // One FFN group of a drained batch, written by the plan kernel.  A group's
-// rows are covered by up to two row-tile families: "big" tiles (256 rows for
-// bf16/fp8 weights, 64 for f32) over rows [0, nbig * big_bm), clamped to n,
-// and "small" 64-row tiles over rows [small_row0, n).
+// rows are covered by up to three row-tile families (bf16 / fp8 weights):
+// "big" 256-row tiles over the full 256-row blocks (plus one more when the
+// remainder exceeds 192 rows), then "medium" 128-row tiles and at most one
+// "small" 64-row tile over the remainder.  f32 weights use the big family
+// alone, with 64-row tiles.  Family f covers rows [row0[f], row0[f] +
+// nrt[f] * height), clamped to n.  t0[stage * 3 + f] is the group's first
+// tile id in family f of a stage (0: gate/up, 1: down).
 struct GroupDesc {
-  int32_t n;           // rows
-  int32_t x_row0;      // first row in x_perm
-  int32_t y_row0;      // first row in h and y
-  int32_t nbig;        // big row tiles
-  int32_t nsmall;      // small row tiles
-  int32_t small_row0;  // first row of the small tiles
-  int32_t t0[4];       // first tile: gate/up big, gate/up small, down big, down small
-  int32_t pad[2];
+  int32_t n;        // rows
+  int32_t x_row0;   // first row in x_perm
+  int32_t y_row0;   // first row in h and y
+  int32_t nrt[3];   // row tiles per family: big, medium, small
+  int32_t row0[3];  // first row of each family
+  int32_t t0[6];    // first tile id per (stage, family)
+  int32_t pad;
 };
-static_assert(sizeof(GroupDesc) == 48, "GroupDesc layout");
+static_assert(sizeof(GroupDesc) == 64, "GroupDesc layout");
 
 // Device error flag bits.
 constexpr int32_t kErrNonFinite = 1;
@@ -63,8 +66,10 @@ constexpr int kMaxGroups = 1024;
 constexpr int kBM = 256;
 constexpr int kBN = 256;
 constexpr int kBK = 64;
-constexpr int kSmallBM = 64;   // small-family tiles (bf16 weights): 64 rows ...
-constexpr int kSmallBN = 128;  // ... x 128 columns (gate/up: 64 features)
+constexpr int kSmallBM = 64;            // small-family tiles: 64 rows ...
+constexpr int kSmallBN = 128;           // ... x 128 columns (gate/up: 64 features)
+constexpr int kMedBM = 128;             // medium-family tiles: 128 rows ...
+constexpr int kMedBN = 128;             // ... x 128 columns
 // f32 path
 constexpr int kBM32 = 64;
 constexpr int kBN32 = 64;
@@ -87,17 +92,18 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
                                int k, int expert, int E, const int32_t* depth_cur,
                                int32_t* depth_nxt, QEntry* q, int64_t q_stride, int32_t* err,
                                hipStream_t s);
-// tile_totals[4]: gate/up big, gate/up small, down big, down small.  nt[4]:
-// column tiles per row tile in the same order.  small_bm = 0 disables the
-// small family (every row in big tiles of big_bm).
+// tile_totals[6] and nt[6] (column tiles per row tile), index stage * 3 +
+// family (stage 0 gate/up, 1 down; family 0 big, 1 medium, 2 small).
+// med_bm = small_bm = 0 disables the two smaller families (every row in big
+// tiles of big_bm).
 // only_expert >= 0: drain that expert's queue alone (every other group gets
 // 0 rows and keeps its queue).  depth is the current half of the layer's
 // depth ping-pong, depth_other the other one; both are cleared for the
 // drained experts.
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
                        int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
-                       int32_t* tile_totals, const int* nt, int big_bm, int small_bm, int32_t* pos,
-                       float* posw, hipStream_t s);
+                       int32_t* tile_totals, const int* nt, int big_bm, int med_bm, int small_bm,
+                       int32_t* pos, float* posw, hipStream_t s);
 // N bounds the routed rows (the exact count is offsets[E] on the device);
 // pos == nullptr skips the (token, slot) -> row map.
 hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,

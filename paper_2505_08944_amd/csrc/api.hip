@@ -108,7 +108,7 @@ bool layout(Ctx& c) {
   c.off_counts = take(sizeof(int32_t) * c.G);
   c.off_offsets = take(sizeof(int32_t) * (c.G + 1));
   c.off_groups = take(sizeof(GroupDesc) * c.G);
-  c.off_tiles = take(sizeof(int32_t) * 4);
+  c.off_tiles = take(sizeof(int32_t) * 6);
   c.off_xp = take((size_t)xrows * d * c.esz);
   c.off_rowtok = take(sizeof(int32_t) * N);
   c.off_roww = take(sizeof(float) * N);
@@ -130,24 +130,27 @@ hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE; }
 
-// Tiling of the FFN launches: nt[4] = column tiles per row tile (gate/up big,
-// gate/up small, down big, down small) and the row-tile heights.  f32 uses
-// 64 x 64 tiles only; bf16 and fp8 weights use 256 x 256 tiles plus the
-// 64 x 128 small family.
-void tiling(const Ctx& c, int nt[4], int* big_bm, int* small_bm) {
+// Tiling of the FFN launches: nt[6] = column tiles per row tile, index
+// stage * 3 + family (stage 0 gate/up, 1 down; family big, medium, small),
+// and the row-tile heights.  f32 uses 64 x 64 tiles only; bf16 and fp8
+// weights use 256 x 256 big tiles, 128 x 128 medium and 64 x 128 small ones.
+void tiling(const Ctx& c, int nt[6], int* big_bm, int* med_bm, int* small_bm) {
   const int d = c.cfg.d_model, f = c.cfg.d_ffn;
   auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
   if (c.cfg.act_dtype == AEP_F32) {
-    nt[0] = nt[1] = cdiv(f, kBN32);
-    nt[2] = nt[3] = cdiv(d, kBN32);
+    nt[0] = nt[1] = nt[2] = cdiv(f, kBN32);
+    nt[3] = nt[4] = nt[5] = cdiv(d, kBN32);
     *big_bm = kBM32;
-    *small_bm = 0;
+    *med_bm = *small_bm = 0;
   } else {
     nt[0] = cdiv(f, kBN / 2);
-    nt[1] = cdiv(f, kSmallBN / 2);
-    nt[2] = cdiv(d, kBN);
-    nt[3] = cdiv(d, kSmallBN);
+    nt[1] = cdiv(f, kMedBN / 2);
+    nt[2] = cdiv(f, kSmallBN / 2);
+    nt[3] = cdiv(d, kBN);
+    nt[4] = cdiv(d, kMedBN);
+    nt[5] = cdiv(d, kSmallBN);
     *big_bm = kBM;
+    *med_bm = kMedBM;
     *small_bm = kSmallBM;
   }
 }
@@ -432,8 +435,8 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   if (L.rows == 0 && !(c->cfg.n_shared > 0 && L.tokens > 0)) return AEP_ERR_EMPTY;
   for (int g = 0; g < c->G; ++g)
     if (!L.have_w[g]) return AEP_ERR_STATE;
-  int nt[4], big_bm, small_bm;
-  tiling(*c, nt, &big_bm, &small_bm);
+  int nt[6], big_bm, med_bm, small_bm;
+  tiling(*c, nt, &big_bm, &med_bm, &small_bm);
   hipStream_t s = as_stream(stream);
   const int E = c->cfg.n_experts, S = c->cfg.n_shared, k = c->cfg.top_k;
   int32_t* counts = c->at<int32_t>(c->off_counts);
@@ -441,8 +444,8 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   int32_t* pos = c->at<int32_t>(c->off_pos);
   float* posw = c->at<float>(c->off_posw);
   if (launch_plan(E, S, L.tokens, k, -1, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
-                  c->at<GroupDesc>(c->off_groups), c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, pos,
-                  posw, s) != hipSuccess)
+                  c->at<GroupDesc>(c->off_groups), c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm,
+                  small_bm, pos, posw, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, L.rows, L.tokens, S > 0, c->tokrow(layer),
@@ -480,15 +483,15 @@ aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batc
   const int64_t nb = std::min(L.bound[expert], L.rows);
   if (nb == 0) return AEP_ERR_EMPTY;
   if (!L.have_w[expert]) return AEP_ERR_STATE;
-  int nt[4], big_bm, small_bm;
-  tiling(*c, nt, &big_bm, &small_bm);
+  int nt[6], big_bm, med_bm, small_bm;
+  tiling(*c, nt, &big_bm, &med_bm, &small_bm);
   hipStream_t s = as_stream(stream);
   const int E = c->cfg.n_experts, k = c->cfg.top_k;
   int32_t* counts = c->at<int32_t>(c->off_counts);
   int32_t* offsets = c->at<int32_t>(c->off_offsets);
   if (launch_plan(E, 0, 0, k, expert, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
                   c->at<GroupDesc>(c->off_groups),
-                  c->at<int32_t>(c->off_tiles), nt, big_bm, small_bm, nullptr, nullptr, s) != hipSuccess)
+                  c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm, small_bm, nullptr, nullptr, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, nb, 0, 0, c->tokrow(layer), c->at<char>(c->off_xp),
@@ -529,14 +532,15 @@ static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, 
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
   if (stage == 1 && !y) return AEP_ERR_INVALID_ARG;
-  int nt[4], big_bm, small_bm;
-  tiling(*c, nt, &big_bm, &small_bm);
+  int nt[6], big_bm, med_bm, small_bm;
+  tiling(*c, nt, &big_bm, &med_bm, &small_bm);
   const int64_t E = c->cfg.n_experts, S = c->cfg.n_shared, G = E + S;
   const int64_t N = batch->n_routed, T = batch->n_tokens;
-  // bound on tiles: every group's rows in big tiles, plus at most 3 small row
-  // tiles per group
+  // bound on tiles: every group's rows in big tiles, plus at most 2 medium
+  // and 1 small row tiles per group
   const int64_t big_rows = N / big_bm + std::min<int64_t>(E, N) + S * ((T + big_bm - 1) / big_bm);
-  const int64_t mt = big_rows * nt[stage == 0 ? 0 : 2] + (small_bm ? 3 * G * nt[stage == 0 ? 1 : 3] : 0);
+  const int* ns = nt + 3 * stage;
+  const int64_t mt = big_rows * ns[0] + (small_bm ? G * (2 * (int64_t)ns[1] + ns[2]) : 0);
   if (mt > INT32_MAX) return AEP_ERR_UNSUPPORTED;
   return dev(launch_ffn(stage, c->cfg.act_dtype, c->cfg.w_dtype, c->at<GroupDesc>(c->off_groups),
                         c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles), (int)mt,

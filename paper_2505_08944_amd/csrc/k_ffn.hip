@@ -112,6 +112,21 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xf) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
 }
 
+// Wait until at most MUL * per loads are outstanding, per in [LO, HI] (the
+// wave's loads per K step; the immediate must be a constant, hence the
+// uniform branch ladder).
+template <int MUL, int LO, int HI>
+__device__ __forceinline__ void wait_steps(int per) {
+  if constexpr (MUL == 0 || LO == HI) {
+    wait_vmcnt<MUL * LO>();
+  } else {
+    if (per <= LO)
+      wait_vmcnt<MUL * LO>();
+    else
+      wait_steps<MUL, LO + 1, HI>(per);
+  }
+}
+
 // One output tile of BM rows x BN columns (gate/up: BN/2 features of gate and
 // the same BN/2 of up) at row m0 of group gd, column tile nti.  Four waves in
 // a 2 x 2 grid, each owning a (BM/2) x (BN/2) block of 32 x 32 MFMA
@@ -173,6 +188,13 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
   const uint16_t* abase = A + (int64_t)(arow0 + m0) * K;
   const int alast = gd.n - 1 - m0;
+  // A load blocks of this wave that hold rows of the group: blocks past the
+  // group's end are not loaded (their LDS rows hold stale data, their outputs
+  // are never stored), which saves the activation traffic of ragged and cold
+  // tiles.  Every K step of the tile issues the same number of loads per wave.
+  const int na_eff = __builtin_amdgcn_readfirstlane(
+      max(0, min(kNA, (alast + 1 - wave * kNA * kRplA + kRplA - 1) / kRplA)));
+  const int per_step = na_eff + kNB;
   uint32_t aoff[kNA], boff[kNB];
 #pragma unroll
   for (int i = 0; i < kNA; ++i)
@@ -198,7 +220,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     const uint32_t sa_ = lds_base + (st_) * kStageB + wave * kNA * 1024;                          \
     const uint32_t sb_ = lds_base + (st_) * kStageB + kTileA + wave * kNB * 1024;                 \
     _Pragma("unroll") for (int i = 0; i < kNA; ++i)                                              \
-        dload16(abase + aoff[i] + (kt_) * BKS, sa_ + i * 1024);                                  \
+        if (i < na_eff) dload16(abase + aoff[i] + (kt_) * BKS, sa_ + i * 1024);                  \
     _Pragma("unroll") for (int i = 0; i < kNB; ++i)                                              \
         dload16(bmat + boff[i] + (kt_) * kRowB, sb_ + i * 1024);                                 \
   } while (0)
@@ -285,7 +307,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   __syncthreads();  // every wave is done with the previous tile's LDS
 #pragma unroll
   for (int s = 0; s < kDist; ++s) DL_LOAD(min(s, KT - 1), s);
-  wait_vmcnt<(kDist - 1) * kPerStep>();  // step 0 has landed (this wave's part)
+  wait_steps<kDist - 1, kNB, kPerStep>(per_step);  // step 0 has landed (this wave's part)
   __syncthreads();                       // ... and every wave's part
   // Step kt computes stage kt % STAGES and refills the stage read in step
   // kt - 1 (every wave passed that step's barrier) with step kt + kDist.
@@ -302,7 +324,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       DL_GROUP(st, 1, a1, b1, a0, b0);
       DL_GROUP(st, 2, a0, b0, a1, b1);
       DL_GROUP(st, 3, a1, b1, a0, b0);
-      wait_vmcnt<(kDist - 1) * kPerStep>();  // step kt + 1 has landed
+      wait_steps<kDist - 1, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
       DL_GROUP(nst, 0, a0, b0, a1, b1);
       st = nst;
@@ -318,7 +340,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       DL_LOAD(min(kt + kDist, KT - 1), fst);
       __builtin_amdgcn_sched_barrier(0);
       DL_GROUP8(st, 1, a11, a21, r1, a10, a20, r0);
-      wait_vmcnt<(kDist - 1) * kPerStep>();  // step kt + 1 has landed
+      wait_steps<kDist - 1, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
       DL_GROUP8(nst, 0, a10, a20, r0, a11, a21, r1);
       st = nst;
@@ -396,57 +418,65 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 }
 
 // The FFN launch for bf16 or fp8 weights: every tile of the big family (256
-// rows), then every tile of the small family (64 rows: cold experts and the
-// ragged tails of hot ones), in one persistent grid.  Small tiles come last,
-// so they also fill the tail of the big ones.  Small tiles are 64 rows x 128
-// columns: cold experts are weight-streaming bound, and narrower tiles spread
-// each expert's weights over more CUs.  fp8 stages are smaller (e4m3 B
-// tiles), so the rings are deeper: 3 big / 6 small stages instead of 2 / 4.
+// rows), then the medium (128 rows) and small (64 rows) tiles of the row
+// remainders and of cold experts, in one persistent grid.  The smaller
+// families come last, so they also fill the tail of the big one; cold
+// experts are weight-streaming bound, and narrow tiles spread each expert's
+// weights over more CUs.  fp8 stages are smaller (e4m3 B tiles), so the rings
+// are deeper: 3 big / 6 medium and small stages instead of 2 / 4.
 template <bool FP8>
 constexpr int ring_bytes(int stages, int bm, int bn) {
   return stages * (bm * kBK * 2 + bn * kBK * (FP8 ? 1 : 2));
 }
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
 template <bool GATED, bool FP8>
 __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   constexpr int kBigStages = FP8 ? 3 : 2, kSmallStages = FP8 ? 6 : 4;
-  constexpr int kRingBig = ring_bytes<FP8>(kBigStages, kBM, kBN);
-  constexpr int kRingSmall = ring_bytes<FP8>(kSmallStages, kSmallBM, kSmallBN);
-  constexpr int kRing = kRingBig > kRingSmall ? kRingBig : kRingSmall;
+  constexpr int kRing = cmax(ring_bytes<FP8>(kBigStages, kBM, kBN),
+                             cmax(ring_bytes<FP8>(kSmallStages, kMedBM, kMedBN),
+                                  ring_bytes<FP8>(kSmallStages, kSmallBM, kSmallBN)));
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kRing];
-  __shared__ int32_t t0b[kMaxGroups + 1], t0s[kMaxGroups + 1];
+  __shared__ int32_t t0f[3][kMaxGroups + 1];
   const int tid = threadIdx.x;
   const int G = p.G;
-  const int big_total = p.tile_totals[GATED ? 0 : 2];
-  const int small_total = p.tile_totals[GATED ? 1 : 3];
-  for (int g = tid; g < G; g += 256) {
-    t0b[g] = p.groups[g].t0[GATED ? 0 : 2];
-    t0s[g] = p.groups[g].t0[GATED ? 1 : 3];
-  }
+  const int st3 = GATED ? 0 : 3;
+  const int tot0 = p.tile_totals[st3], tot1 = p.tile_totals[st3 + 1], tot2 = p.tile_totals[st3 + 2];
+  for (int g = tid; g < G; g += 256)
+    for (int f = 0; f < 3; ++f) t0f[f][g] = p.groups[g].t0[st3 + f];
   if (tid == 0) {
-    t0b[G] = big_total;
-    t0s[G] = small_total;
+    t0f[0][G] = tot0;
+    t0f[1][G] = tot1;
+    t0f[2][G] = tot2;
   }
   __syncthreads();
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
   const int nwg = gridDim.x;
   const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
   const int ncol_big = GATED ? (p.n_out + kBN / 2 - 1) / (kBN / 2) : (p.n_out + kBN - 1) / kBN;
-  for (int tile = slot; tile < big_total + small_total; tile += nwg) {
-    if (tile < big_total) {
-      const int g = find_group(t0b, G, tile);
+  for (int tile = slot; tile < tot0 + tot1 + tot2; tile += nwg) {
+    if (tile < tot0) {
+      const int g = find_group(t0f[0], G, tile);
       const GroupDesc gd = p.groups[g];
-      const int local = tile - t0b[g];
+      const int local = tile - t0f[0][g];
       int rt, nti;
-      panel_decode(local, gd.nbig, ncol_big, rt, nti);
+      panel_decode(local, gd.nrt[0], ncol_big, rt, nti);
       dl_tile<GATED, FP8, kBM, kBN, kBigStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
     } else {
-      const int t = tile - big_total;
-      const int g = find_group(t0s, G, t);
+      // medium or small: the row tiles of one column tile are consecutive
+      const bool med = tile < tot0 + tot1;
+      const int f = med ? 1 : 2;
+      const int t = tile - (med ? tot0 : tot0 + tot1);
+      const int g = find_group(t0f[f], G, t);
       const GroupDesc gd = p.groups[g];
-      const int local = t - t0s[g];
-      const int nti = local / gd.nsmall;
-      dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kRing>(
-          p, smem, lds_base, gd, p.wtab[g], nti, gd.small_row0 + (local - nti * gd.nsmall) * kSmallBM);
+      const int local = t - t0f[f][g];
+      const int nti = local / gd.nrt[f];
+      const int ri = local - nti * gd.nrt[f];
+      if (med)
+        dl_tile<GATED, FP8, kMedBM, kMedBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
+                                                                 gd.row0[1] + ri * kMedBM);
+      else
+        dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
+                                                                     gd.row0[2] + ri * kSmallBM);
     }
   }
 }
@@ -461,8 +491,8 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(const FfnParams p) {
   __shared__ int32_t t0s[kMaxGroups + 1];
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
   const int G = p.G;
-  const int total = p.tile_totals[GATED ? 0 : 2];
-  for (int g = tid; g < G; g += 256) t0s[g] = p.groups[g].t0[GATED ? 0 : 2];
+  const int total = p.tile_totals[GATED ? 0 : 3];
+  for (int g = tid; g < G; g += 256) t0s[g] = p.groups[g].t0[GATED ? 0 : 3];
   if (tid == 0) t0s[G] = total;
   __syncthreads();
   const int K = p.K, n_out = p.n_out;
@@ -474,8 +504,8 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(const FfnParams p) {
     const GroupDesc gd = p.groups[g];
     const WeightDesc wd = p.wtab[g];
     const int local = tile - t0s[g];
-    const int nti = local / gd.nbig;
-    const int m0 = (local - nti * gd.nbig) * BM;
+    const int nti = local / gd.nrt[0];
+    const int m0 = (local - nti * gd.nrt[0]) * BM;
     const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
     const int lr = tid >> 2, lk = (tid & 3) * 4;
     const float* asrc = A + (int64_t)(arow0 + min(m0 + lr, gd.n - 1)) * K + lk;

@@ -2,8 +2,8 @@
 //
 // plan (one workgroup): reads the drained layer's per-expert queue depths
 // (or one expert's, for a single-expert drain), writes counts / exclusive-scan
-// offsets / the FFN group table (row bases and tile ranges), resets the
-// drained queue depths to zero and clears the (token, slot) -> row map.
+// offsets / the FFN group table (row-tile families and tile ranges), resets
+// the drained queue depths to zero and clears the (token, slot) -> row map.
 //
 // gather: one wave per batch row.  A routed row finds its expert by binary
 // search over the offsets, reads its queue entry and copies the referenced
@@ -15,15 +15,18 @@
 
 namespace aep {
 
+struct NT6 {
+  int v[6];
+};
+
 __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, int k,
                                                     int only_expert, int32_t* __restrict__ depth,
                                                     int32_t* __restrict__ depth_other,
                                                     int32_t* __restrict__ counts,
                                                     int32_t* __restrict__ offsets,
                                                     GroupDesc* __restrict__ groups,
-                                                    int32_t* __restrict__ tile_totals, int nt0,
-                                                    int nt1, int nt2, int nt3, int big_bm,
-                                                    int small_bm,
+                                                    int32_t* __restrict__ tile_totals,
+                                                    NT6 nt, int big_bm, int med_bm, int small_bm,
                                                     int32_t* __restrict__ pos,
                                                     float* __restrict__ posw) {
   __shared__ int32_t cnt[kMaxGroups];
@@ -36,45 +39,45 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
     int N = 0;
     for (int g = 0; g < E; ++g) N += cnt[g];
     int off = 0;
-    int t[4] = {0, 0, 0, 0};
+    int t[6] = {0, 0, 0, 0, 0, 0};
     for (int g = 0; g < G; ++g) {
       const int n = cnt[g];
-      int nbig, nsmall = 0;
+      int nrt[3] = {0, 0, 0};
+      const int full = n / big_bm, r = n - full * big_bm;
       if (small_bm == 0) {
-        nbig = (n + big_bm - 1) / big_bm;
+        nrt[0] = (n + big_bm - 1) / big_bm;
+      } else if (r > big_bm - big_bm / 4) {
+        // a remainder filling more than 3/4 of a big tile takes one more
+        nrt[0] = full + 1;
       } else {
-        // Full big tiles, then the remainder in small tiles unless it would
-        // take more than 3 of them (then one more big tile is as cheap).
-        const int full = n / big_bm, r = n - full * big_bm;
-        nbig = full;
-        if (r > 3 * small_bm)
-          nbig += 1;
-        else
-          nsmall = (r + small_bm - 1) / small_bm;
+        // full big tiles, then full medium tiles; what is left goes to one
+        // more medium tile above small_bm rows, else to one small tile
+        nrt[0] = full;
+        nrt[1] = r / med_bm;
+        const int rem = r - nrt[1] * med_bm;
+        if (rem > small_bm)
+          nrt[1] += 1;
+        else if (rem > 0)
+          nrt[2] = 1;
       }
       GroupDesc gd;
       gd.n = n;
       gd.x_row0 = g < E ? off : N;
       gd.y_row0 = off;
-      gd.nbig = nbig;
-      gd.nsmall = nsmall;
-      gd.small_row0 = (n / big_bm) * big_bm;
-      gd.t0[0] = t[0];
-      gd.t0[1] = t[1];
-      gd.t0[2] = t[2];
-      gd.t0[3] = t[3];
-      gd.pad[0] = gd.pad[1] = 0;
+      gd.row0[0] = 0;
+      gd.row0[1] = full * big_bm;
+      gd.row0[2] = full * big_bm + (small_bm ? (r / med_bm) * med_bm : 0);
+      for (int f = 0; f < 3; ++f) gd.nrt[f] = nrt[f];
+      for (int i = 0; i < 6; ++i) gd.t0[i] = t[i];
+      gd.pad = 0;
       groups[g] = gd;
       counts[g] = n;
       offsets[g] = off;
       off += n;
-      t[0] += nbig * nt0;
-      t[1] += nsmall * nt1;
-      t[2] += nbig * nt2;
-      t[3] += nsmall * nt3;
+      for (int i = 0; i < 6; ++i) t[i] += nrt[i % 3] * nt.v[i];
     }
     offsets[G] = off;
-    for (int i = 0; i < 4; ++i) tile_totals[i] = t[i];
+    for (int i = 0; i < 6; ++i) tile_totals[i] = t[i];
   }
   // The drained queues are empty again, in both halves of the depth
   // ping-pong: whichever half the next append reads starts from zero (so a
@@ -136,10 +139,12 @@ __global__ __launch_bounds__(256) void gather_kernel(
 
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
                        int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
-                       int32_t* tile_totals, const int* nt, int big_bm, int small_bm, int32_t* pos,
-                       float* posw, hipStream_t s) {
+                       int32_t* tile_totals, const int* nt, int big_bm, int med_bm, int small_bm,
+                       int32_t* pos, float* posw, hipStream_t s) {
+  NT6 n6;
+  for (int i = 0; i < 6; ++i) n6.v[i] = nt[i];
   plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, only_expert, depth, depth_other, counts, offsets, groups,
-                                  tile_totals, nt[0], nt[1], nt[2], nt[3], big_bm, small_bm, pos, posw);
+                                  tile_totals, n6, big_bm, med_bm, small_bm, pos, posw);
   return hipGetLastError();
 }
 
