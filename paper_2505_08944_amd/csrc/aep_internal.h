@@ -34,8 +34,8 @@ static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 // One FFN group of a drained batch, written by the plan kernel.  A group's
 // rows are covered by up to three row-tile families (bf16 / fp8 weights):
 // "big" 256-row tiles over the full 256-row blocks (plus one more when the
-// remainder exceeds 192 rows), then "medium" 128-row tiles and at most one
-// "small" 64-row tile over the remainder.  f32 weights use the big family
+// remainder exceeds 192 rows, unless the batch is cold), then "medium"
+// 128-row tiles and at most one "small" 64-row tile over the remainder.  f32 weights use the big family
 // alone, with 64-row tiles.  Family f covers rows [row0[f], row0[f] +
 // nrt[f] * height), clamped to n.  t0[stage * 3 + f] is the group's first
 // tile id in family f of a stage (0: gate/up, 1: down).
@@ -95,7 +95,8 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
 // tile_totals[6] and nt[6] (column tiles per row tile), index stage * 3 +
 // family (stage 0 gate/up, 1 down; family 0 big, 1 medium, 2 small).
 // med_bm = small_bm = 0 disables the two smaller families (every row in big
-// tiles of big_bm).
+// tiles of big_bm).  num_cu: a batch with fewer full big gate/up tiles than
+// CUs puts no remainder in a big tile.
 // only_expert >= 0: drain that expert's queue alone (every other group gets
 // 0 rows and keeps its queue).  depth is the current half of the layer's
 // depth ping-pong, depth_other the other one; both are cleared for the
@@ -103,7 +104,7 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
                        int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
                        int32_t* tile_totals, const int* nt, int big_bm, int med_bm, int small_bm,
-                       int32_t* pos, float* posw, hipStream_t s);
+                       int num_cu, int32_t* pos, float* posw, hipStream_t s);
 // N bounds the routed rows (the exact count is offsets[E] on the device);
 // pos == nullptr skips the (token, slot) -> row map.
 hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,

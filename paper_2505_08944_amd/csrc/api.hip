@@ -445,7 +445,7 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   float* posw = c->at<float>(c->off_posw);
   if (launch_plan(E, S, L.tokens, k, -1, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
                   c->at<GroupDesc>(c->off_groups), c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm,
-                  small_bm, pos, posw, s) != hipSuccess)
+                  small_bm, c->num_cu, pos, posw, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, L.rows, L.tokens, S > 0, c->tokrow(layer),
@@ -491,7 +491,8 @@ aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batc
   int32_t* offsets = c->at<int32_t>(c->off_offsets);
   if (launch_plan(E, 0, 0, k, expert, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
                   c->at<GroupDesc>(c->off_groups),
-                  c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm, small_bm, nullptr, nullptr, s) != hipSuccess)
+                  c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm, small_bm, c->num_cu, nullptr, nullptr,
+                  s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, nb, 0, 0, c->tokrow(layer), c->at<char>(c->off_xp),

@@ -27,6 +27,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
                                                     GroupDesc* __restrict__ groups,
                                                     int32_t* __restrict__ tile_totals,
                                                     NT6 nt, int big_bm, int med_bm, int small_bm,
+                                                    int num_cu,
                                                     int32_t* __restrict__ pos,
                                                     float* __restrict__ posw) {
   __shared__ int32_t cnt[kMaxGroups];
@@ -38,6 +39,12 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
   if (tid == 0) {
     int N = 0;
     for (int g = 0; g < E; ++g) N += cnt[g];
+    // A batch whose full big tiles do not fill one round of the grid is
+    // cold: its remainders go to medium tiles only (a few long big tiles
+    // would be the critical path of a weight-streaming launch).
+    int64_t full_tiles = 0;
+    for (int g = 0; g < G; ++g) full_tiles += (int64_t)(cnt[g] / big_bm) * nt.v[0];
+    const bool cold = full_tiles < num_cu;
     int off = 0;
     int t[6] = {0, 0, 0, 0, 0, 0};
     for (int g = 0; g < G; ++g) {
@@ -46,7 +53,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, 
       const int full = n / big_bm, r = n - full * big_bm;
       if (small_bm == 0) {
         nrt[0] = (n + big_bm - 1) / big_bm;
-      } else if (r > big_bm - big_bm / 4) {
+      } else if (!cold && r > big_bm - big_bm / 4) {
         // a remainder filling more than 3/4 of a big tile takes one more
         nrt[0] = full + 1;
       } else {
@@ -140,11 +147,11 @@ __global__ __launch_bounds__(256) void gather_kernel(
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
                        int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
                        int32_t* tile_totals, const int* nt, int big_bm, int med_bm, int small_bm,
-                       int32_t* pos, float* posw, hipStream_t s) {
+                       int num_cu, int32_t* pos, float* posw, hipStream_t s) {
   NT6 n6;
   for (int i = 0; i < 6; ++i) n6.v[i] = nt[i];
   plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, only_expert, depth, depth_other, counts, offsets, groups,
-                                  tile_totals, n6, big_bm, med_bm, small_bm, pos, posw);
+                                  tile_totals, n6, big_bm, med_bm, small_bm, num_cu, pos, posw);
   return hipGetLastError();
 }
 
