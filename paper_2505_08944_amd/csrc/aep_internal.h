@@ -57,6 +57,8 @@ constexpr int32_t kErrSlotRange = 4;
 constexpr int32_t kErrCollision = 8;
 
 constexpr int kRouteThreads = 256;
+constexpr int kRouteLanes = 8;                              // lanes per token in the router
+constexpr int kRouteTokens = kRouteThreads / kRouteLanes;   // tokens per router workgroup
 constexpr int kMaxRouteExperts = 64;
 constexpr int kMaxTopK = 8;
 constexpr int kMaxGroups = 1024;

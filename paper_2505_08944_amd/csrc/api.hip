@@ -104,7 +104,7 @@ bool layout(Ctx& c) {
   c.off_ridx = take(sizeof(int32_t) * N);
   c.off_rw = take(sizeof(float) * N);
   c.off_rrank = take(sizeof(int32_t) * N);
-  c.off_blockcnt = take(sizeof(int32_t) * ((T + kRouteThreads - 1) / kRouteThreads) * E);
+  c.off_blockcnt = take(sizeof(int32_t) * ((T + kRouteTokens - 1) / kRouteTokens) * E);
   c.off_counts = take(sizeof(int32_t) * c.G);
   c.off_offsets = take(sizeof(int32_t) * (c.G + 1));
   c.off_groups = take(sizeof(GroupDesc) * c.G);

@@ -155,7 +155,6 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   constexpr int kNA = BM / kRplA / 4;         // direct loads per wave per K step: A
   constexpr int kNB = BN / kRplB / 4;         // ... and B
   constexpr int kTileA = BM * kRowA, kStageB = BM * kRowA + BN * kRowB;
-  constexpr int kDist = STAGES - 1;
   constexpr int kPerStep = kNA + kNB;
   constexpr int kLd = BN / 2 + 8;             // epilogue staging row stride (bf16)
   static_assert(MI >= 1 && NI >= 2 && NI % 2 == 0, "wave tile");
@@ -163,7 +162,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   static_assert(!GATED || kNB * kRplB == TN / 2, "a wave's B rows are all gate or all up rows");
   static_assert(STAGES * kStageB <= CAP, "ring must fit the shared buffer");
   static_assert(BM * kLd * 2 <= CAP, "epilogue staging must fit");
-  static_assert((kDist - 1) * kPerStep < 64, "vmcnt range");
+  static_assert((STAGES - 1) * kPerStep < 64, "vmcnt range");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -306,26 +305,27 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   wait_vmcnt<0>();
   __syncthreads();  // every wave is done with the previous tile's LDS
 #pragma unroll
-  for (int s = 0; s < kDist; ++s) DL_LOAD(min(s, KT - 1), s);
-  wait_steps<kDist - 1, kNB, kPerStep>(per_step);  // step 0 has landed (this wave's part)
-  __syncthreads();                       // ... and every wave's part
-  // Step kt computes stage kt % STAGES and refills the stage read in step
-  // kt - 1 (every wave passed that step's barrier) with step kt + kDist.
-  // Past the last step the loads repeat the last step (never read).
+  for (int s = 0; s < STAGES; ++s) DL_LOAD(min(s, KT - 1), s);
+  wait_steps<STAGES - 1, kNB, kPerStep>(per_step);  // step 0 has landed (this wave's part)
+  __syncthreads();                                  // ... and every wave's part
+  // Step kt computes stage kt % STAGES.  Its last operand reads come before
+  // the barrier that ends the step, so right after that barrier the stage
+  // is refilled with step kt + STAGES: a step's loads have STAGES - 1 whole
+  // steps of MFMA work to land.  Past the last step the loads repeat the
+  // last step (never read).
   if constexpr (!FP8) {
     bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
     DL_READ(0, 0, a0, b0);
     int st = 0;
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st + 1 == STAGES ? 0 : st + 1;
-      const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
-      DL_LOAD(min(kt + kDist, KT - 1), fst);
-      __builtin_amdgcn_sched_barrier(0);
       DL_GROUP(st, 1, a1, b1, a0, b0);
       DL_GROUP(st, 2, a0, b0, a1, b1);
       DL_GROUP(st, 3, a1, b1, a0, b0);
-      wait_steps<kDist - 1, kNB, kPerStep>(per_step);  // step kt + 1 has landed
+      wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
+      DL_LOAD(min(kt + STAGES, KT - 1), st);
+      __builtin_amdgcn_sched_barrier(0);
       DL_GROUP(nst, 0, a0, b0, a1, b1);
       st = nst;
     }
@@ -336,12 +336,11 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     int st = 0;
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st + 1 == STAGES ? 0 : st + 1;
-      const int fst = st + kDist >= STAGES ? st + kDist - STAGES : st + kDist;
-      DL_LOAD(min(kt + kDist, KT - 1), fst);
-      __builtin_amdgcn_sched_barrier(0);
       DL_GROUP8(st, 1, a11, a21, r1, a10, a20, r0);
-      wait_steps<kDist - 1, kNB, kPerStep>(per_step);  // step kt + 1 has landed
+      wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
+      DL_LOAD(min(kt + STAGES, KT - 1), st);
+      __builtin_amdgcn_sched_barrier(0);
       DL_GROUP8(nst, 0, a10, a20, r0, a11, a21, r1);
       st = nst;
     }
@@ -392,7 +391,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
           if constexpr (GATED) {
             const float gv = FP8 ? acc[i][j][r] * sg : acc[i][j][r];
             const float uv = FP8 ? acc[i][j + NI / 2][r] * su : acc[i][j + NI / 2][r];
-            v = __fdividef(gv, 1.f + __expf(-gv)) * uv;
+            v = gv * __builtin_amdgcn_rcpf(1.f + __expf(-gv)) * uv;
           } else {
             v = FP8 ? acc[i][j][r] * sg : acc[i][j][r];
           }

@@ -1,9 +1,10 @@
 // Executor re-batch kernels: drain plan + gather.
 //
-// plan (one workgroup): reads the drained layer's per-expert queue depths
-// (or one expert's, for a single-expert drain), writes counts / exclusive-scan
-// offsets / the FFN group table (row-tile families and tile ranges), resets
-// the drained queue depths to zero and clears the (token, slot) -> row map.
+// plan: workgroup 0 reads the drained layer's per-expert queue depths (or one
+// expert's, for a single-expert drain) with one thread per group, and writes
+// counts / exclusive-scan offsets / the FFN group table (row-tile families
+// and tile ranges) from workgroup-wide scans; it resets the drained queue
+// depths to zero.  All workgroups clear the (token, slot) -> row map.
 //
 // gather: one wave per batch row.  A routed row finds its expert by binary
 // search over the offsets, reads its queue entry and copies the referenced
@@ -11,6 +12,8 @@
 // one contiguous coalesced stream); lane 0 records the row's token and gate
 // weight and the (token, slot) -> row map.  Shared-expert rows copy every
 // token's row in id order.
+#include <algorithm>
+
 #include "aep_internal.h"
 
 namespace aep {
@@ -19,80 +22,135 @@ struct NT6 {
   int v[6];
 };
 
-__global__ __launch_bounds__(1024) void plan_kernel(int E, int S, int n_tokens, int k,
-                                                    int only_expert, int32_t* __restrict__ depth,
-                                                    int32_t* __restrict__ depth_other,
-                                                    int32_t* __restrict__ counts,
-                                                    int32_t* __restrict__ offsets,
-                                                    GroupDesc* __restrict__ groups,
-                                                    int32_t* __restrict__ tile_totals,
-                                                    NT6 nt, int big_bm, int med_bm, int small_bm,
-                                                    int num_cu,
-                                                    int32_t* __restrict__ pos,
-                                                    float* __restrict__ posw) {
-  __shared__ int32_t cnt[kMaxGroups];
-  const int tid = threadIdx.x;
-  const int G = E + S;
-  for (int g = tid; g < G; g += blockDim.x)
-    cnt[g] = g < E ? (only_expert < 0 || g == only_expert ? depth[g] : 0) : n_tokens;
+constexpr int kPlanThreads = 1024;
+
+// Exclusive scan of NV ints per thread over a workgroup of kPlanThreads
+// threads (inclusive wave scans with shuffles, then a scan of the wave
+// totals by NV threads); `total` receives the workgroup sums.  wsum holds
+// kPlanThreads / 64 + 1 rows.
+template <int NV>
+__device__ __forceinline__ void plan_block_scan(int (&v)[NV], int (&total)[NV],
+                                                int32_t (*wsum)[NV]) {
+  constexpr int kWaves = kPlanThreads / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) inc[i] = v[i];
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int y = __shfl_up(inc[i], off);
+      if (lane >= off) inc[i] += y;
+    }
+  }
+  if (lane == 63)
+#pragma unroll
+    for (int i = 0; i < NV; ++i) wsum[wave][i] = inc[i];
   __syncthreads();
-  if (tid == 0) {
-    int N = 0;
-    for (int g = 0; g < E; ++g) N += cnt[g];
+  if (threadIdx.x < NV) {
+    const int i = threadIdx.x;
+    int acc = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      const int x = wsum[w][i];
+      wsum[w][i] = acc;
+      acc += x;
+    }
+    wsum[kWaves][i] = acc;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    v[i] = wsum[wave][i] + inc[i] - v[i];
+    total[i] = wsum[kWaves][i];
+  }
+  __syncthreads();
+}
+
+// Workgroup 0 plans the drain, one thread per group; every workgroup clears
+// its share of the (token, slot) -> row map.
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_tokens, int k,
+                                                            int only_expert, int32_t* __restrict__ depth,
+                                                            int32_t* __restrict__ depth_other,
+                                                            int32_t* __restrict__ counts,
+                                                            int32_t* __restrict__ offsets,
+                                                            GroupDesc* __restrict__ groups,
+                                                            int32_t* __restrict__ tile_totals,
+                                                            NT6 nt, int big_bm, int med_bm, int small_bm,
+                                                            int num_cu,
+                                                            int32_t* __restrict__ pos,
+                                                            float* __restrict__ posw) {
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0) {
+    __shared__ int32_t wsum2[kPlanThreads / 64 + 1][2];
+    __shared__ int32_t wsum7[kPlanThreads / 64 + 1][7];
+    const int G = E + S;
+    const int g = tid;
+    const bool real = g < G;
+    const int n = !real ? 0 : g < E ? (only_expert < 0 || g == only_expert ? depth[g] : 0) : n_tokens;
+    const int full = n / big_bm, r = n - full * big_bm;
+    // routed rows, and the full big gate/up tiles of the whole batch
+    int a[2] = {g < E ? n : 0, full * nt.v[0]};
+    int sum2[2];
+    plan_block_scan<2>(a, sum2, wsum2);
+    const int N = sum2[0];
     // A batch whose full big tiles do not fill one round of the grid is
     // cold: its remainders go to medium tiles only (a few long big tiles
     // would be the critical path of a weight-streaming launch).
-    int64_t full_tiles = 0;
-    for (int g = 0; g < G; ++g) full_tiles += (int64_t)(cnt[g] / big_bm) * nt.v[0];
-    const bool cold = full_tiles < num_cu;
-    int off = 0;
-    int t[6] = {0, 0, 0, 0, 0, 0};
-    for (int g = 0; g < G; ++g) {
-      const int n = cnt[g];
-      int nrt[3] = {0, 0, 0};
-      const int full = n / big_bm, r = n - full * big_bm;
-      if (small_bm == 0) {
-        nrt[0] = (n + big_bm - 1) / big_bm;
-      } else if (!cold && r > big_bm - big_bm / 4) {
-        // a remainder filling more than 3/4 of a big tile takes one more
-        nrt[0] = full + 1;
-      } else {
-        // full big tiles, then full medium tiles; what is left goes to one
-        // more medium tile above small_bm rows, else to one small tile
-        nrt[0] = full;
-        nrt[1] = r / med_bm;
-        const int rem = r - nrt[1] * med_bm;
-        if (rem > small_bm)
-          nrt[1] += 1;
-        else if (rem > 0)
-          nrt[2] = 1;
-      }
+    const bool cold = sum2[1] < num_cu;
+    int nrt[3] = {0, 0, 0};
+    if (small_bm == 0) {
+      nrt[0] = (n + big_bm - 1) / big_bm;
+    } else if (!cold && r > big_bm - big_bm / 4) {
+      // a remainder filling more than 3/4 of a big tile takes one more
+      nrt[0] = full + 1;
+    } else {
+      // full big tiles, then full medium tiles; what is left goes to one
+      // more medium tile above small_bm rows, else to one small tile
+      nrt[0] = full;
+      nrt[1] = r / med_bm;
+      const int rem = r - nrt[1] * med_bm;
+      if (rem > small_bm)
+        nrt[1] += 1;
+      else if (rem > 0)
+        nrt[2] = 1;
+    }
+    int b[7];
+    b[0] = n;
+#pragma unroll
+    for (int i = 0; i < 6; ++i) b[1 + i] = nrt[i % 3] * nt.v[i];
+    int sum7[7];
+    plan_block_scan<7>(b, sum7, wsum7);
+    if (real) {
       GroupDesc gd;
       gd.n = n;
-      gd.x_row0 = g < E ? off : N;
-      gd.y_row0 = off;
+      gd.x_row0 = g < E ? b[0] : N;
+      gd.y_row0 = b[0];
       gd.row0[0] = 0;
       gd.row0[1] = full * big_bm;
       gd.row0[2] = full * big_bm + (small_bm ? (r / med_bm) * med_bm : 0);
+#pragma unroll
       for (int f = 0; f < 3; ++f) gd.nrt[f] = nrt[f];
-      for (int i = 0; i < 6; ++i) gd.t0[i] = t[i];
+#pragma unroll
+      for (int i = 0; i < 6; ++i) gd.t0[i] = b[1 + i];
       gd.pad = 0;
       groups[g] = gd;
       counts[g] = n;
-      offsets[g] = off;
-      off += n;
-      for (int i = 0; i < 6; ++i) t[i] += nrt[i % 3] * nt.v[i];
+      offsets[g] = b[0];
     }
-    offsets[G] = off;
-    for (int i = 0; i < 6; ++i) tile_totals[i] = t[i];
+    if (g == 0) {
+      offsets[G] = sum7[0];
+#pragma unroll
+      for (int i = 0; i < 6; ++i) tile_totals[i] = sum7[1 + i];
+    }
+    // The drained queues are empty again, in both halves of the depth
+    // ping-pong: whichever half the next append reads starts from zero (so a
+    // captured drain step replays correctly whatever the parity of its
+    // appends).  Every read of depth above precedes the scans' barriers.
+    if (g < E && (only_expert < 0 || g == only_expert)) depth[g] = depth_other[g] = 0;
   }
-  // The drained queues are empty again, in both halves of the depth
-  // ping-pong: whichever half the next append reads starts from zero (so a
-  // captured drain step replays correctly whatever the parity of its appends).
-  for (int e = tid; e < E; e += blockDim.x)
-    if (only_expert < 0 || e == only_expert) depth[e] = depth_other[e] = 0;
   const int64_t nk = (int64_t)n_tokens * k;
-  for (int64_t i = tid; i < nk; i += blockDim.x) {
+  for (int64_t i = (int64_t)blockIdx.x * kPlanThreads + tid; i < nk; i += (int64_t)gridDim.x * kPlanThreads) {
     pos[i] = -1;
     posw[i] = 0.f;
   }
@@ -150,7 +208,10 @@ hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32
                        int num_cu, int32_t* pos, float* posw, hipStream_t s) {
   NT6 n6;
   for (int i = 0; i < 6; ++i) n6.v[i] = nt[i];
-  plan_kernel<<<1, 1024, 0, s>>>(E, S, n_tokens, k, only_expert, depth, depth_other, counts, offsets, groups,
+  static_assert(kMaxGroups <= kPlanThreads, "one plan thread per group");
+  const int64_t nk = (int64_t)n_tokens * k;
+  const unsigned nb = (unsigned)std::min<int64_t>(256, std::max<int64_t>(1, (nk + 4 * kPlanThreads - 1) / (4 * kPlanThreads)));
+  plan_kernel<<<nb, kPlanThreads, 0, s>>>(E, S, n_tokens, k, only_expert, depth, depth_other, counts, offsets, groups,
                                   tile_totals, n6, big_bm, med_bm, small_bm, num_cu, pos, posw);
   return hipGetLastError();
 }
