@@ -30,6 +30,7 @@ import numpy as np
 
 METRIC = "expert-layer tokens/sec + % MFMA peak (hot) / % HBM BW (cold), Zipf-skewed"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_SCLK_GHZ = 2.4     # clock the published MFMA peaks assume
 PEAK_HBM_GBS = 8000.0
 
 
@@ -49,6 +50,8 @@ def parse():
                     help="host threads for input generation")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the cold-expert (weight-streaming) measurements")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time the step alone: skip the cold, hot-expert and 8-layer drain measurements")
     ap.add_argument("--sweep", action="store_true",
                     help="also sweep rows per expert (16..256) on same-shape expert groups of >= 1 GB")
     ap.add_argument("--sched-sim", action="store_true",
@@ -325,6 +328,22 @@ def main():
     elapsed = time.perf_counter() - t0
     ctx.sync()  # device error flag must be clear
 
+    # shader clock the gate/up launch runs at (clock probe, outside the timed
+    # steps): cycles over 100 MHz ticks, summed over the workgroups
+    clk = torch.zeros((torch.cuda.get_device_properties(0).multi_processor_count, 2), dtype=torch.int64,
+                      device=dev)
+    for x, lg in zip(xs, lgs):
+        ctx.route_enqueue(0, x, lg)
+    b = ctx.rebatch(0)
+    ctx.set_clock_probe(clk)
+    ctx.expert_gate_up(b)
+    ctx.set_clock_probe(None)
+    ctx.release(b)
+    torch.cuda.synchronize()
+    ck = clk.cpu().numpy().astype(np.float64)
+    ck = ck[ck[:, 1] > 0]
+    sclk_ghz = float(ck[:, 0].sum() / (ck[:, 1].sum() / 100e6) / 1e9) if len(ck) else None
+
     stage_names = ["route_enqueue", "rebatch", "gate_up", "down", "combine"]
     stage_ms = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(K)]))
                 for j, n in enumerate(stage_names)}
@@ -353,7 +372,10 @@ def main():
                 "traffic_detail": tr,
                 "algorithmic_bytes": gu_bytes,
                 "per_launch": {"flops": gu_flops, "rows": n_rows, "flops_per_row": 4 * w.d * w.f,
-                               "avg_ms": round(stage_ms["gate_up"], 4)}}
+                               "avg_ms": round(stage_ms["gate_up"], 4)},
+                "sclk_ghz": None if sclk_ghz is None else round(sclk_ghz, 3),
+                "frac_at_sclk": None if sclk_ghz is None else
+                round(achieved / (PEAK_BF16_TFLOPS * sclk_ghz / PEAK_SCLK_GHZ), 4)}
 
     res = {
         "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
@@ -370,11 +392,19 @@ def main():
         "setup_s": round(t_gen, 1),
     }
 
-    del ctx, wdev, xs, lgs, y, out
+    del ctx, xs, lgs, y, out
     torch.cuda.empty_cache()
 
-    # ---------------------------------------------------------------- cold experts
-    if not args.no_cold:
+    # ------------------------------------------- hot experts, 8-layer drain, cold
+    if not args.step_only:
+        mixtral = args.workload == "c2"
+        if mixtral:
+            res["drain_c5"] = drain_measurement(wdev, args.threads)
+        res["hot"] = hot_measurements(max(counts[:w.E]) if mixtral else 0,
+                                      res["drain_c5"]["hottest_queue_rows"] if mixtral else 0)
+    del wdev
+    torch.cuda.empty_cache()
+    if not args.no_cold and not args.step_only:
         res["cold"] = cold_measurements(args)
 
     # ---------------------------------------------------------------- CPU oracle
@@ -454,6 +484,100 @@ def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0, flush="read"):
     del ctx, W, rows, flush_buf
     torch.cuda.empty_cache()
     return t, byts, 6.0 * d * f * N
+
+
+def hot_measurements(c2_hot_rows: int, drain_hot_rows: int):
+    """MFMA side of the metric: one expert's whole queue as a single group
+    (gate/up + down), caches warm: the hottest queue of the Mixtral-style
+    layer, the EP share's 4096-row expert (bf16 and fp8 weights) and the
+    hottest queue of the 8-layer drain (row counts measured on the device)."""
+    out = {}
+    cases = []
+    if c2_hot_rows:
+        cases.append(("mixtral_hottest", c2_hot_rows, 4096, 14336, "bf16"))
+    cases += [("ep_share_4096", 4096, 4096, 2048, "bf16"), ("ep_share_4096", 4096, 4096, 2048, "fp8")]
+    if drain_hot_rows:
+        cases.append(("drain_hottest", drain_hot_rows, 4096, 14336, "bf16"))
+    for name, n, d, f, wdt in cases:
+        t, byts, fl = time_rows_ffn([n], d, f, wdt, reps=5, flush="none")
+        out[f"{name}_d{d}_f{f}_{wdt}"] = {"rows": n, "ms": round(t * 1e3, 4), "tflops": round(fl / t / 1e12, 1),
+                                           "mfma_frac": round(fl / t / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    return out
+
+
+def drain_measurement(c2_weights, threads: int, reps: int = 3):
+    """The asynchronous 8-layer drain: 8 MoE layers at the Mixtral-style shape
+    (layer weights: the layer's 8 experts drawn from the same 8 synthetic
+    experts, rotated per layer, each (layer, expert) its own copy), 0..8192
+    tokens per layer, 32768 in total.  One pass routes every layer's fragments
+    into its mu-queues, then repeatedly picks the layer with the most queued
+    rows (host, no sync), re-batches it, runs its experts and combines, until
+    every queue is empty.  Wall time of the pass, host picks included."""
+    import torch
+    import synth
+    import paper_2505_08944_amd as aep
+    w = synth.workload("c5")
+    dev = torch.device("cuda", 0)
+    ctx = aep.Context(w.n_layers, w.E, w.d, w.f, w.k, max_tokens_per_layer=max(max(w.tokens), 1))
+    wdev = []
+    for l in range(w.n_layers):
+        for e in range(w.E):
+            src = synth.weight_source(w, l, e)[2]
+            t = [m.clone() for m in c2_weights[src][:3]]
+            ctx.set_expert_weights(l, e, *t)
+            wdev.append(t)
+    frags = []
+    for l in range(w.n_layers):
+        fl = []
+        for f in synth.layer_fragments(w, l):
+            x = torch.from_numpy(np.ascontiguousarray(f["x"]).view(np.int16)).view(torch.bfloat16).to(dev)
+            fl.append((x, torch.from_numpy(np.ascontiguousarray(f["logits"])).to(dev)))
+        frags.append(fl)
+    ys = {l: torch.empty((2 * w.tokens[l], w.d), dtype=torch.bfloat16, device=dev) for l in range(w.n_layers)}
+    outs = {l: torch.empty((w.tokens[l], w.d), dtype=torch.bfloat16, device=dev) for l in range(w.n_layers)}
+
+    def one_pass():
+        for l in range(w.n_layers):
+            for x, lg in frags[l]:
+                ctx.route_enqueue(l, x, lg)
+        order = []
+        while (l := ctx.pick_layer("mtfs")) is not None:
+            order.append(l)
+            b = ctx.rebatch(l)
+            ctx.expert_gate_up(b)
+            ctx.expert_down(b, ys[l])
+            ctx.combine(b, ys[l], outs[l])
+            ctx.release(b)
+        return order
+
+    one_pass()
+    torch.cuda.synchronize()
+    ctx.sync()
+    hottest = 0
+    for l in range(w.n_layers):
+        for x, lg in frags[l]:
+            ctx.route_enqueue(l, x, lg)
+        hottest = max(hottest, int(ctx.expert_counts(l).max()))
+    while (l := ctx.pick_layer("mtfs")) is not None:
+        ctx.release(ctx.rebatch(l))
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        order = one_pass()
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t0)
+    ctx.sync()
+    T = sum(w.tokens)
+    t = float(np.median(times))
+    flops = 6.0 * w.d * w.f * 2 * T
+    res = {"workload": w.description, "layers": w.n_layers, "tokens": T, "layer_tokens": list(w.tokens),
+           "order": order, "hottest_queue_rows": hottest, "ms": round(t * 1e3, 3),
+           "tokens_per_s": round(T / t, 1), "ffn_tflops": round(flops / t / 1e12, 1), "reps": reps}
+    del ctx, wdev, frags, ys, outs
+    torch.cuda.empty_cache()
+    return res
 
 
 def cold_measurements(args):

@@ -337,6 +337,17 @@ aep_status aep_release_batch(void* ctx, aep_batch* batch);
 /* Wait for `stream`, then report (and clear) the device error flag. */
 aep_status aep_sync(void* ctx, void* stream);
 
+/* Clock probe (instrumentation).  With d_buf a device array of 2 * n_pairs
+ * uint64, every later bf16 / fp8-weight FFN launch of this context writes,
+ * for each workgroup w < n_pairs, d_buf[2w] = shader-clock cycles
+ * (s_memtime) and d_buf[2w+1] = ticks of the 100 MHz real-time counter
+ * (s_memrealtime) elapsed in that workgroup; their ratio is the clock the
+ * kernel ran at.  A launch overwrites the previous one's values; workgroups
+ * of a launch are at most the CU count.  d_buf = NULL (or n_pairs <= 0)
+ * turns the probe off (the default).  The f32 path records nothing.  The
+ * buffer is borrowed and must stay valid while the probe is on. */
+aep_status aep_set_clock_probe(void* ctx, uint64_t* d_buf, int32_t n_pairs);
+
 /* Utility: decode n OCP e4m3fn codes (device) to bf16 (device); exact. */
 aep_status aep_fp8_e4m3_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stream);
 

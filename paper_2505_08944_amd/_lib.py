@@ -88,6 +88,7 @@ _SIG = {
     "aep_combine": (ctypes.c_int, [_P, ctypes.POINTER(Batch), _P, _P, _P]),
     "aep_release_batch": (ctypes.c_int, [_P, ctypes.POINTER(Batch)]),
     "aep_sync": (ctypes.c_int, [_P, _P]),
+    "aep_set_clock_probe": (ctypes.c_int, [_P, _P, _I32]),
     "aep_fp8_e4m3_to_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
     "aep_route_enqueue_ids": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _P, _P, _P, _P]),
     "aep_rebatch_expert": (ctypes.c_int, [_P, _I32, _I32, ctypes.POINTER(Batch), _P]),

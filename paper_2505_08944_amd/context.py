@@ -273,6 +273,18 @@ class Context:
     def sync(self) -> None:
         L.check(self.lib.aep_sync(self.h, _stream()), "aep_sync")
 
+    def set_clock_probe(self, buf: Optional[torch.Tensor]) -> None:
+        """Record per-workgroup (shader-clock cycles, 100 MHz ticks) of later
+        FFN launches into buf (device int64 [n, 2]); None turns it off."""
+        if buf is None:
+            L.check(self.lib.aep_set_clock_probe(self.h, None, 0), "aep_set_clock_probe")
+            return
+        if buf.device.type != "cuda" or buf.dtype != torch.int64 or buf.dim() != 2 or buf.shape[1] != 2 \
+                or not buf.is_contiguous():
+            raise ValueError("clock probe buffer: contiguous device int64 [n, 2]")
+        self._clock_buf = buf
+        L.check(self.lib.aep_set_clock_probe(self.h, buf.data_ptr(), buf.shape[0]), "aep_set_clock_probe")
+
     def run_layer(self, layer: int, y: Optional[torch.Tensor] = None,
                   out: Optional[torch.Tensor] = None) -> torch.Tensor:
         """Drain one layer: re-batch, expert FFN, combine; returns out [n_tokens, d]."""

@@ -122,9 +122,12 @@ hipError_t launch_pool_release(int act_dtype, float* pool, int32_t* live, int32_
                                void* out, int32_t* ready, int d, hipStream_t s);
 // stage 0: gate/up (xp -> h), stage 1: down (h -> y); max_tiles bounds the
 // stage's tile count (the exact count is on the device).
+// clk != nullptr: workgroup w < clk_n writes its elapsed (s_memtime,
+// s_memrealtime) ticks to clk[2w], clk[2w + 1] (bf16 / fp8 weights only).
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
                       const WeightDesc* wtab, int G, const int32_t* tile_totals, int max_tiles,
-                      const void* xp, void* h, void* y, int d, int f, int num_cu, hipStream_t s);
+                      const void* xp, void* h, void* y, int d, int f, int num_cu,
+                      unsigned long long* clk, int clk_n, hipStream_t s);
 hipError_t launch_combine(int act_dtype, const void* y, int64_t N, int n_tokens, int S, int k,
                           const int32_t* pos, const float* posw, void* out, int d, hipStream_t s);
 hipError_t launch_fp8_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, hipStream_t s);

@@ -50,6 +50,8 @@ struct Ctx {
   int num_cu = 0;
   std::vector<LayerState> layers;
   std::vector<WeightDesc> wtab_host;  // [layer][group]
+  unsigned long long* clk = nullptr;  // clock probe (aep_set_clock_probe)
+  int clk_n = 0;
   bool batch_out = false;
   bool batch_expert = false;  // the outstanding batch is a single-expert drain
   uint64_t epoch = 0;
@@ -546,7 +548,16 @@ static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, 
   return dev(launch_ffn(stage, c->cfg.act_dtype, c->cfg.w_dtype, c->at<GroupDesc>(c->off_groups),
                         c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles), (int)mt,
                         c->ws + c->off_xp, c->ws + c->off_h, y, c->cfg.d_model, c->cfg.d_ffn, c->num_cu,
-                        as_stream(stream)));
+                        c->clk, c->clk_n, as_stream(stream)));
+}
+
+aep_status aep_set_clock_probe(void* ctx, uint64_t* d_buf, int32_t n_pairs) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return AEP_ERR_INVALID_ARG;
+  const bool on = d_buf != nullptr && n_pairs > 0;
+  c->clk = on ? reinterpret_cast<unsigned long long*>(d_buf) : nullptr;
+  c->clk_n = on ? n_pairs : 0;
+  return AEP_OK;
 }
 
 aep_status aep_expert_gate_up(void* ctx, const aep_batch* batch, void* stream) {

@@ -46,6 +46,8 @@ struct FfnParams {
   int G;
   int K;      // reduction length: d (gate/up) or f (down)
   int n_out;  // output columns: f (gate/up) or d (down)
+  unsigned long long* clk;  // clock probe (nullptr: off)
+  int clk_n;
 };
 
 // Accumulator layout of v_mfma_f32_32x32x16_bf16: lane l, register r holds
@@ -436,6 +438,12 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
                                   ring_bytes<FP8>(kSmallStages, kSmallBM, kSmallBN)));
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kRing];
   __shared__ int32_t t0f[3][kMaxGroups + 1];
+  const bool probe = p.clk != nullptr && (int)blockIdx.x < p.clk_n;
+  unsigned long long clk0 = 0, rt0 = 0;
+  if (probe) {
+    clk0 = __builtin_amdgcn_s_memtime();
+    rt0 = __builtin_amdgcn_s_memrealtime();
+  }
   const int tid = threadIdx.x;
   const int G = p.G;
   const int st3 = GATED ? 0 : 3;
@@ -476,6 +484,13 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       else
         dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
                                                                      gd.row0[2] + ri * kSmallBM);
+    }
+  }
+  if (probe) {
+    const unsigned long long clk1 = __builtin_amdgcn_s_memtime(), rt1 = __builtin_amdgcn_s_memrealtime();
+    if (tid == 0) {
+      p.clk[2 * blockIdx.x] = clk1 - clk0;
+      p.clk[2 * blockIdx.x + 1] = rt1 - rt0;
     }
   }
 }
@@ -581,10 +596,11 @@ static int grid_for(int max_tiles, int cap) {
 
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
                       const WeightDesc* wtab, int G, const int32_t* tile_totals, int max_tiles,
-                      const void* xp, void* h, void* y, int d, int f, int num_cu, hipStream_t s) {
+                      const void* xp, void* h, void* y, int d, int f, int num_cu,
+                      unsigned long long* clk, int clk_n, hipStream_t s) {
   if (max_tiles <= 0) return hipSuccess;
-  const FfnParams p = stage == 0 ? FfnParams{groups, wtab, tile_totals, xp, h, G, d, f}
-                                 : FfnParams{groups, wtab, tile_totals, h, y, G, f, d};
+  const FfnParams p = stage == 0 ? FfnParams{groups, wtab, tile_totals, xp, h, G, d, f, clk, clk_n}
+                                 : FfnParams{groups, wtab, tile_totals, h, y, G, f, d, clk, clk_n};
   if (act_dtype == 0) {
     const int grid = grid_for(max_tiles, 4 * num_cu);
     if (stage == 0)
