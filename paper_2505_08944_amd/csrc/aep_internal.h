@@ -35,10 +35,13 @@ static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 // rows are covered by up to three row-tile families (bf16 / fp8 weights):
 // "big" 256-row tiles over the full 256-row blocks (plus one more when the
 // remainder exceeds 192 rows, unless the batch is cold), then "medium"
-// 128-row tiles and at most one "small" 64-row tile over the remainder.  f32 weights use the big family
-// alone, with 64-row tiles.  Family f covers rows [row0[f], row0[f] +
-// nrt[f] * height), clamped to n.  t0[stage * 3 + f] is the group's first
-// tile id in family f of a stage (0: gate/up, 1: down).
+// 128-row tiles and at most one "small" 64-row tile over the remainder.  In
+// a cold batch (tile_totals[6] != 0) family 1 is "tall" instead: one
+// 256-row tile (kTallBM) over a remainder above 64 rows, so a cold expert's
+// weights are streamed once.  f32 weights use the big family alone, with
+// 64-row tiles.  Family f covers rows [row0[f], row0[f] + nrt[f] * height),
+// clamped to n.  t0[stage * 3 + f] is the group's first tile id in family f
+// of a stage (0: gate/up, 1: down).
 struct GroupDesc {
   int32_t n;        // rows
   int32_t x_row0;   // first row in x_perm
@@ -72,6 +75,7 @@ constexpr int kSmallBM = 64;            // small-family tiles: 64 rows ...
 constexpr int kSmallBN = 128;           // ... x 128 columns (gate/up: 64 features)
 constexpr int kMedBM = 128;             // medium-family tiles: 128 rows ...
 constexpr int kMedBN = 128;             // ... x 128 columns
+constexpr int kTallBM = 256;            // family 1 of a cold batch: 256 rows x kMedBN columns
 // f32 path
 constexpr int kBM32 = 64;
 constexpr int kBN32 = 64;
@@ -94,8 +98,9 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
                                int k, int expert, int E, const int32_t* depth_cur,
                                int32_t* depth_nxt, QEntry* q, int64_t q_stride, int32_t* err,
                                hipStream_t s);
-// tile_totals[6] and nt[6] (column tiles per row tile), index stage * 3 +
-// family (stage 0 gate/up, 1 down; family 0 big, 1 medium, 2 small).
+// tile_totals[7] and nt[6] (column tiles per row tile), index stage * 3 +
+// family (stage 0 gate/up, 1 down; family 0 big, 1 medium, 2 small);
+// tile_totals[6] = 1 for a cold batch (family 1 tiles are kTallBM rows).
 // med_bm = small_bm = 0 disables the two smaller families (every row in big
 // tiles of big_bm).  num_cu: a batch with fewer full big gate/up tiles than
 // CUs puts no remainder in a big tile.

@@ -419,8 +419,8 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 }
 
 // The FFN launch for bf16 or fp8 weights: every tile of the big family (256
-// rows), then the medium (128 rows) and small (64 rows) tiles of the row
-// remainders and of cold experts, in one persistent grid.  The smaller
+// rows), then the medium (128 rows; 256 in a cold batch) and small (64 rows)
+// tiles of the row remainders and of cold experts, in one persistent grid.  The smaller
 // families come last, so they also fill the tail of the big one; cold
 // experts are weight-streaming bound, and narrow tiles spread each expert's
 // weights over more CUs.  fp8 stages are smaller (e4m3 B tiles), so the rings
@@ -432,8 +432,9 @@ constexpr int ring_bytes(int stages, int bm, int bn) {
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 template <bool GATED, bool FP8>
 __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
-  constexpr int kBigStages = FP8 ? 3 : 2, kSmallStages = FP8 ? 6 : 4;
-  constexpr int kRing = cmax(ring_bytes<FP8>(kBigStages, kBM, kBN),
+  constexpr int kBigStages = FP8 ? 3 : 2, kSmallStages = FP8 ? 6 : 4, kTallStages = 3;
+  constexpr int kRing = cmax(cmax(ring_bytes<FP8>(kBigStages, kBM, kBN),
+                                  ring_bytes<FP8>(kTallStages, kTallBM, kMedBN)),
                              cmax(ring_bytes<FP8>(kSmallStages, kMedBM, kMedBN),
                                   ring_bytes<FP8>(kSmallStages, kSmallBM, kSmallBN)));
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kRing];
@@ -448,6 +449,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   const int G = p.G;
   const int st3 = GATED ? 0 : 3;
   const int tot0 = p.tile_totals[st3], tot1 = p.tile_totals[st3 + 1], tot2 = p.tile_totals[st3 + 2];
+  const bool tall = p.tile_totals[6] != 0;  // cold batch: family 1 tiles are kTallBM rows
   for (int g = tid; g < G; g += 256)
     for (int f = 0; f < 3; ++f) t0f[f][g] = p.groups[g].t0[st3 + f];
   if (tid == 0) {
@@ -478,7 +480,10 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const int local = t - t0f[f][g];
       const int nti = local / gd.nrt[f];
       const int ri = local - nti * gd.nrt[f];
-      if (med)
+      if (med && tall)
+        dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
+                                                                 gd.row0[1] + ri * kTallBM);
+      else if (med)
         dl_tile<GATED, FP8, kMedBM, kMedBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
                                                                  gd.row0[1] + ri * kMedBM);
       else

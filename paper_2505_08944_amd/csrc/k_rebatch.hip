@@ -99,9 +99,19 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
     // would be the critical path of a weight-streaming launch).
     const bool cold = sum2[1] < num_cu;
     int nrt[3] = {0, 0, 0};
+    int fam1_rows = 0;  // rows covered by family 1 before the small tile
     if (small_bm == 0) {
       nrt[0] = (n + big_bm - 1) / big_bm;
-    } else if (!cold && r > big_bm - big_bm / 4) {
+    } else if (cold) {
+      // full big tiles; the remainder takes one tall tile (kTallBM rows:
+      // the expert's weights are read once) above small_bm rows, else one
+      // small tile
+      nrt[0] = full;
+      if (r > small_bm)
+        nrt[1] = 1;
+      else if (r > 0)
+        nrt[2] = 1;
+    } else if (r > big_bm - big_bm / 4) {
       // a remainder filling more than 3/4 of a big tile takes one more
       nrt[0] = full + 1;
     } else {
@@ -114,6 +124,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
         nrt[1] += 1;
       else if (rem > 0)
         nrt[2] = 1;
+      fam1_rows = (r / med_bm) * med_bm;
     }
     int b[7];
     b[0] = n;
@@ -128,7 +139,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
       gd.y_row0 = b[0];
       gd.row0[0] = 0;
       gd.row0[1] = full * big_bm;
-      gd.row0[2] = full * big_bm + (small_bm ? (r / med_bm) * med_bm : 0);
+      gd.row0[2] = full * big_bm + fam1_rows;
 #pragma unroll
       for (int f = 0; f < 3; ++f) gd.nrt[f] = nrt[f];
 #pragma unroll
@@ -142,6 +153,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
       offsets[G] = sum7[0];
 #pragma unroll
       for (int i = 0; i < 6; ++i) tile_totals[i] = sum7[1 + i];
+      tile_totals[6] = small_bm != 0 && cold ? 1 : 0;
     }
     // The drained queues are empty again, in both halves of the depth
     // ping-pong: whichever half the next append reads starts from zero (so a
