@@ -36,12 +36,12 @@ static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 // "big" 256-row tiles over the full 256-row blocks (plus one more when the
 // remainder exceeds 192 rows, unless the batch is cold), then "medium"
 // 128-row tiles and at most one "small" 64-row tile over the remainder.  In
-// a cold batch (tile_totals[6] != 0) family 1 is "tall" instead: one
-// 256-row tile (kTallBM) over a remainder above 64 rows, so a cold expert's
-// weights are streamed once.  f32 weights use the big family alone, with
-// 64-row tiles.  Family f covers rows [row0[f], row0[f] + nrt[f] * height),
-// clamped to n.  t0[stage * 3 + f] is the group's first tile id in family f
-// of a stage (0: gate/up, 1: down).
+// a cold batch a remainder above 128 rows takes one "tall" 256-row tile
+// (kTallBM) in family 1 instead (h1 = kTallBM), so a cold expert's weights
+// are streamed once.  f32 weights use the big family alone, with 64-row
+// tiles.  Family f covers rows [row0[f], row0[f] + nrt[f] * height), clamped
+// to n (family 1 height: h1).  t0[stage * 3 + f] is the group's first tile id
+// in family f of a stage (0: gate/up, 1: down).
 struct GroupDesc {
   int32_t n;        // rows
   int32_t x_row0;   // first row in x_perm
@@ -49,7 +49,7 @@ struct GroupDesc {
   int32_t nrt[3];   // row tiles per family: big, medium, small
   int32_t row0[3];  // first row of each family
   int32_t t0[6];    // first tile id per (stage, family)
-  int32_t pad;
+  int32_t h1;       // rows per family-1 tile: kMedBM, or kTallBM in a cold batch
 };
 static_assert(sizeof(GroupDesc) == 64, "GroupDesc layout");
 
@@ -98,9 +98,8 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
                                int k, int expert, int E, const int32_t* depth_cur,
                                int32_t* depth_nxt, QEntry* q, int64_t q_stride, int32_t* err,
                                hipStream_t s);
-// tile_totals[7] and nt[6] (column tiles per row tile), index stage * 3 +
-// family (stage 0 gate/up, 1 down; family 0 big, 1 medium, 2 small);
-// tile_totals[6] = 1 for a cold batch (family 1 tiles are kTallBM rows).
+// tile_totals[6] and nt[6] (column tiles per row tile), index stage * 3 +
+// family (stage 0 gate/up, 1 down; family 0 big, 1 medium, 2 small).
 // med_bm = small_bm = 0 disables the two smaller families (every row in big
 // tiles of big_bm).  num_cu: a batch with fewer full big gate/up tiles than
 // CUs puts no remainder in a big tile.

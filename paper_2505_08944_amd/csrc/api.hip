@@ -110,7 +110,7 @@ bool layout(Ctx& c) {
   c.off_counts = take(sizeof(int32_t) * c.G);
   c.off_offsets = take(sizeof(int32_t) * (c.G + 1));
   c.off_groups = take(sizeof(GroupDesc) * c.G);
-  c.off_tiles = take(sizeof(int32_t) * 8);
+  c.off_tiles = take(sizeof(int32_t) * 6);
   c.off_xp = take((size_t)xrows * d * c.esz);
   c.off_rowtok = take(sizeof(int32_t) * N);
   c.off_roww = take(sizeof(float) * N);

@@ -419,8 +419,9 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 }
 
 // The FFN launch for bf16 or fp8 weights: every tile of the big family (256
-// rows), then the medium (128 rows; 256 in a cold batch) and small (64 rows)
-// tiles of the row remainders and of cold experts, in one persistent grid.  The smaller
+// rows), then the medium (128 rows; 256 for a cold expert's remainder above
+// 128 rows) and small (64 rows) tiles of the row remainders and of cold
+// experts, in one persistent grid.  The smaller
 // families come last, so they also fill the tail of the big one; cold
 // experts are weight-streaming bound, and narrow tiles spread each expert's
 // weights over more CUs.  fp8 stages are smaller (e4m3 B tiles), so the rings
@@ -449,7 +450,6 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   const int G = p.G;
   const int st3 = GATED ? 0 : 3;
   const int tot0 = p.tile_totals[st3], tot1 = p.tile_totals[st3 + 1], tot2 = p.tile_totals[st3 + 2];
-  const bool tall = p.tile_totals[6] != 0;  // cold batch: family 1 tiles are kTallBM rows
   for (int g = tid; g < G; g += 256)
     for (int f = 0; f < 3; ++f) t0f[f][g] = p.groups[g].t0[st3 + f];
   if (tid == 0) {
@@ -480,7 +480,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const int local = t - t0f[f][g];
       const int nti = local / gd.nrt[f];
       const int ri = local - nti * gd.nrt[f];
-      if (med && tall)
+      if (med && gd.h1 == kTallBM)
         dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
                                                                  gd.row0[1] + ri * kTallBM);
       else if (med)

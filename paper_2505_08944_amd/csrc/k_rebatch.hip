@@ -100,17 +100,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
     const bool cold = sum2[1] < num_cu;
     int nrt[3] = {0, 0, 0};
     int fam1_rows = 0;  // rows covered by family 1 before the small tile
+    int h1 = med_bm;    // rows per family-1 tile
     if (small_bm == 0) {
       nrt[0] = (n + big_bm - 1) / big_bm;
-    } else if (cold) {
-      // full big tiles; the remainder takes one tall tile (kTallBM rows:
-      // the expert's weights are read once) above small_bm rows, else one
-      // small tile
+    } else if (cold && r > med_bm) {
+      // full big tiles; a remainder above one medium tile takes one tall
+      // tile (kTallBM rows: the expert's weights are read once)
       nrt[0] = full;
-      if (r > small_bm)
-        nrt[1] = 1;
-      else if (r > 0)
-        nrt[2] = 1;
+      nrt[1] = 1;
+      h1 = kTallBM;
     } else if (r > big_bm - big_bm / 4) {
       // a remainder filling more than 3/4 of a big tile takes one more
       nrt[0] = full + 1;
@@ -144,7 +142,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
       for (int f = 0; f < 3; ++f) gd.nrt[f] = nrt[f];
 #pragma unroll
       for (int i = 0; i < 6; ++i) gd.t0[i] = b[1 + i];
-      gd.pad = 0;
+      gd.h1 = h1;
       groups[g] = gd;
       counts[g] = n;
       offsets[g] = b[0];
@@ -153,7 +151,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
       offsets[G] = sum7[0];
 #pragma unroll
       for (int i = 0; i < 6; ++i) tile_totals[i] = sum7[1 + i];
-      tile_totals[6] = small_bm != 0 && cold ? 1 : 0;
     }
     // The drained queues are empty again, in both halves of the depth
     // ping-pong: whichever half the next append reads starts from zero (so a
