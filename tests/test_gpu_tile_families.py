@@ -1,0 +1,71 @@
+"""GPU parity of every row-tile choice the plan makes, on explicit per-expert
+queue depths (rows mode), against the oracle element by element.
+
+Cold batch (its full 256-row tiles do not fill one round of the grid): a
+remainder above 128 rows takes one tall 256-row tile, 65..128 rows one medium
+tile, 1..64 rows one small tile.  Warm batch: a remainder above 192 rows takes
+one more big tile, otherwise medium tiles and at most one small tile.  The
+depths below put at least one expert on each branch (and exact multiples of
+256, and empty experts), for bf16 and fp8 weights."""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_helpers import BF16_RTOL, assert_close, log, make_context, to_dev, to_host, upload_weights
+
+pytestmark = pytest.mark.gpu
+
+COLD = [300, 200, 100, 40, 1, 256, 0, 129]          # big+small, tall, medium, small, small, big, -, tall
+WARM = [2100, 230, 150, 300, 260, 0, 512, 193]       # 8 big+small, big, medium+small, big+small, big+small,
+                                                     # -, 2 big, big
+
+
+def _rows(w, depths, seed):
+    g = np.random.default_rng(seed)
+    N = int(sum(depths))
+    tok = g.permutation(N).astype(np.int32)
+    gw = g.random(N, dtype=np.float32)
+    x = synth.round_to_bf16_bits(g.standard_normal((N, w.d), dtype=np.float32))
+    per, r0 = [], 0
+    for n in depths:
+        per.append({"x": x[r0:r0 + n], "token_ids": tok[r0:r0 + n], "gate_w": gw[r0:r0 + n]})
+        r0 += n
+    return N, per
+
+
+@pytest.mark.parametrize("kind,wdt", [("cold", "bf16"), ("cold", "fp8"), ("warm", "bf16"), ("warm", "fp8")])
+def test_tile_families_match_oracle(kind, wdt):
+    depths = COLD if kind == "cold" else WARM
+    # warm: f = 8192 gives 64 big gate/up column tiles, so 8 + 2 + 1 + 1 + 1
+    # full 256-row blocks fill more than one round of 256 CUs
+    f = 320 if kind == "cold" else 8192
+    w = synth.Workload(f"fam_{kind}_{wdt}", 110, d=256, f=f, E=len(depths), k=1, zipf_s=1.0, mode="rows",
+                       depth_max=max(depths), wdt=wdt)
+    N, per = _rows(w, depths, 11 if kind == "cold" else 12)
+    log(f"case {kind}/{wdt}: depths {depths}, d={w.d} f={w.f}")
+    ws = synth.all_expert_weights(w, 0, threads=4)
+    ctx = make_context(w, max_tokens=N)
+    dev_w = upload_weights(ctx, w, 0, ws)
+    lq = oracle.LayerQueues(w.E, 1)
+    keep = []
+    for e, ex in enumerate(per):
+        if depths[e] == 0:
+            continue
+        t = (to_dev(ex["x"], "bf16"), to_dev(ex["token_ids"], "i32"), to_dev(ex["gate_w"], "f32"))
+        keep.append(t)
+        ctx.enqueue_rows(0, e, *t, N)
+        lq.enqueue_rows(e, ex["x"], ex["token_ids"], ex["gate_w"], N)
+    b = ctx.rebatch(0)
+    y = ctx.expert_ffn(b)
+    ref = oracle.moe_layer(lq, ws, "bf16", wdt)
+    assert np.array_equal(to_host(b.counts()), ref["batch"].counts)
+    st = assert_close(oracle.bf16_to_f64(to_host(y)), ref["y"], BF16_RTOL, f"{kind}/{wdt} y")
+    log(f"case {kind}/{wdt}: y {st}")
+    ctx.release(b)
+    ctx.sync()
+    del ctx, dev_w, keep
