@@ -9,9 +9,10 @@
 // gather: one wave per batch row.  A routed row finds its expert by binary
 // search over the offsets, reads its queue entry and copies the referenced
 // row (16-byte vector loads/stores, the whole wave on one row, so each row is
-// one contiguous coalesced stream); lane 0 records the row's token and gate
-// weight and the (token, slot) -> row map.  Shared-expert rows copy every
-// token's row in id order.
+// one contiguous coalesced stream; up to 4 loads per lane in flight before
+// the stores); lane 0 records the row's token and gate weight and the
+// (token, slot) -> row map.  Shared-expert rows copy every token's row in id
+// order.
 #include <algorithm>
 
 #include "aep_internal.h"
@@ -205,10 +206,24 @@ __global__ __launch_bounds__(256) void gather_kernel(
   } else {
     src = reinterpret_cast<const uint4*>(tok_row[r - N]);
   }
-  uint4* dst = reinterpret_cast<uint4*>(xp + r * row_bytes);
+  // all of a pass's loads are issued before its stores (the source rows are
+  // global memory; the stores cannot alias them)
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  typedef const __attribute__((address_space(1))) v4u* gsrc_t;
+  const gsrc_t gsrc = (gsrc_t)src;
+  v4u* dst = reinterpret_cast<v4u*>(xp + r * row_bytes);
   const int nchunk = (int)(row_bytes >> 4);
-#pragma unroll 8
-  for (int c = lane; c < nchunk; c += 64) dst[c] = src[c];
+  constexpr int kB = 4;  // 16-byte chunks per lane per pass
+  int c0 = 0;
+  for (; c0 + 64 * kB <= nchunk; c0 += 64 * kB) {
+    // a full pass: every load is issued before the first store
+    v4u v[kB];
+#pragma unroll
+    for (int i = 0; i < kB; ++i) v[i] = gsrc[c0 + lane + 64 * i];
+#pragma unroll
+    for (int i = 0; i < kB; ++i) dst[c0 + lane + 64 * i] = v[i];
+  }
+  for (int c = c0 + lane; c < nchunk; c += 64) dst[c] = gsrc[c];  // the row's tail
 }
 
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,

@@ -144,8 +144,18 @@ __global__ __launch_bounds__(kRouteThreads) void append_kernel(
     // per expert
     const int e = tid % kMaxRouteExperts, p = tid / kMaxRouteExperts;
     int acc = 0;
-    if (e < E)
-      for (int b = p; b < (int)blockIdx.x; b += kParts) acc += blockcnt[(int64_t)b * E + e];
+    if (e < E) {
+      // 8 independent loads per round
+      int b = p;
+      for (; b + 7 * kParts < (int)blockIdx.x; b += 8 * kParts) {
+        int v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = blockcnt[(int64_t)(b + i * kParts) * E + e];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc += v[i];
+      }
+      for (; b < (int)blockIdx.x; b += kParts) acc += blockcnt[(int64_t)b * E + e];
+    }
     part[p][e] = acc;
   }
   __syncthreads();
