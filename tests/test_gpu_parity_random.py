@@ -1,0 +1,60 @@
+"""GPU parity on seeded random layer shapes: routing, queues and gathered rows
+bit-exact, expert outputs and the combined output within tolerance, against
+the oracle.  The shapes are drawn once from a fixed seed and cover the
+corners the fixed cases do not: one expert, k = E, one token, fragments of
+one token, d and ffn of 64, odd expert counts, shared experts with fp8 and
+f32, no renormalisation."""
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_helpers import (BF16_RTOL, F32_RTOL, assert_close, check_routing_and_queues, log, make_context,
+                         oracle_routed_layer, run_routed_layer, upload_weights)
+
+pytestmark = pytest.mark.gpu
+
+
+def _cases():
+    g = np.random.default_rng(250508944)
+    fixed = [
+        dict(d=64, f=64, E=1, k=1, S=0, T=1, n_frag=1, fmt=("bf16", "bf16"), renorm=True),
+        dict(d=128, f=192, E=5, k=5, S=0, T=37, n_frag=4, fmt=("bf16", "fp8"), renorm=False),
+        dict(d=64, f=128, E=64, k=8, S=1, T=9, n_frag=3, fmt=("bf16", "bf16"), renorm=True),
+        dict(d=192, f=64, E=3, k=2, S=2, T=130, n_frag=2, fmt=("f32", "f32"), renorm=True),
+    ]
+    out = list(fixed)
+    for _ in range(10):
+        E = int(g.integers(1, 65))
+        out.append(dict(d=int(g.choice([64, 128, 192, 256, 320])), f=int(g.choice([64, 128, 192, 320, 448])),
+                        E=E, k=int(g.integers(1, min(E, 8) + 1)), S=int(g.choice([0, 0, 1, 2])),
+                        T=int(g.integers(1, 600)), n_frag=int(g.integers(1, 5)),
+                        fmt=[("bf16", "bf16"), ("bf16", "fp8"), ("f32", "f32")][int(g.integers(0, 3))],
+                        renorm=bool(g.integers(0, 2))))
+    return out
+
+
+CASES = _cases()
+
+
+@pytest.mark.parametrize("i", range(len(CASES)))
+def test_random_shape_matches_oracle(i):
+    c = CASES[i]
+    act, wdt = c["fmt"]
+    w = synth.Workload(f"rand{i}", 300 + i, d=c["d"], f=c["f"], E=c["E"], k=c["k"], S=c["S"],
+                       zipf_s=1.1, act=act, wdt=wdt, tokens=(c["T"],), n_frag=c["n_frag"], renorm=c["renorm"])
+    log(f"case rand{i}: T={c['T']} in {c['n_frag']} d={c['d']} f={c['f']} E={c['E']}+{c['S']} k={c['k']} "
+        f"{act}/{wdt} renorm={c['renorm']}")
+    frags = synth.layer_fragments(w, 0)
+    ws = synth.all_expert_weights(w, 0, threads=4)
+    ctx = make_context(w)
+    dev = upload_weights(ctx, w, 0, ws)
+    got = run_routed_layer(ctx, w, 0, frags)
+    ref = oracle_routed_layer(w, frags, ws)
+    check_routing_and_queues(w, got, ref)
+    rtol = F32_RTOL if act == "f32" else BF16_RTOL
+    sy = assert_close(oracle.act_to_f64(got["y"], act), ref["y"], rtol, f"rand{i} y")
+    so = assert_close(oracle.act_to_f64(got["out"], act), ref["out"], rtol, f"rand{i} out")
+    log(f"case rand{i}: y {sy}  out {so}")
+    del ctx, dev
