@@ -42,16 +42,20 @@ static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 // tiles.  Family f covers rows [row0[f], row0[f] + nrt[f] * height), clamped
 // to n (family 1 height: h1).  t0[stage * 3 + f] is the group's first tile id
 // in family f of a stage (0: gate/up, 1: down).
+// Row tiles of one group, per FFN stage (0: gate/up, 1: down): the two
+// stages may split a group's remainder rows differently.
 struct GroupDesc {
-  int32_t n;        // rows
-  int32_t x_row0;   // first row in x_perm
-  int32_t y_row0;   // first row in h and y
-  int32_t nrt[3];   // row tiles per family: big, medium, small
-  int32_t row0[3];  // first row of each family
-  int32_t t0[6];    // first tile id per (stage, family)
-  int32_t h1;       // rows per family-1 tile: kMedBM, or kTallBM in a cold batch
+  int32_t n;          // rows
+  int32_t x_row0;     // first row in x_perm
+  int32_t y_row0;     // first row in h and y
+  int32_t t0[6];      // first tile id per (stage, family)
+  int32_t nrt[2][3];  // row tiles per (stage, family): big, medium (or tall), small
+  int32_t row1[2];    // first row of family 1 per stage (family 0 starts at row 0)
+  int32_t row2[2];    // first row of family 2 per stage
+  int32_t h1[2];      // rows per family-1 tile per stage: kMedBM, or kTallBM in a cold batch
+  int32_t pad[3];
 };
-static_assert(sizeof(GroupDesc) == 64, "GroupDesc layout");
+static_assert(sizeof(GroupDesc) == 96, "GroupDesc layout");
 
 // Device error flag bits.
 constexpr int32_t kErrNonFinite = 1;

@@ -448,7 +448,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   }
   const int tid = threadIdx.x;
   const int G = p.G;
-  const int st3 = GATED ? 0 : 3;
+  const int stage = GATED ? 0 : 1, st3 = 3 * stage;
   const int tot0 = p.tile_totals[st3], tot1 = p.tile_totals[st3 + 1], tot2 = p.tile_totals[st3 + 2];
   for (int g = tid; g < G; g += 256)
     for (int f = 0; f < 3; ++f) t0f[f][g] = p.groups[g].t0[st3 + f];
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const GroupDesc gd = p.groups[g];
       const int local = tile - t0f[0][g];
       int rt, nti;
-      panel_decode(local, gd.nrt[0], ncol_big, rt, nti);
+      panel_decode(local, gd.nrt[stage][0], ncol_big, rt, nti);
       dl_tile<GATED, FP8, kBM, kBN, kBigStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
     } else {
       // medium or small: the row tiles of one column tile are consecutive
@@ -478,17 +478,17 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const int g = find_group(t0f[f], G, t);
       const GroupDesc gd = p.groups[g];
       const int local = t - t0f[f][g];
-      const int nti = local / gd.nrt[f];
-      const int ri = local - nti * gd.nrt[f];
-      if (med && gd.h1 == kTallBM)
+      const int nti = local / gd.nrt[stage][f];
+      const int ri = local - nti * gd.nrt[stage][f];
+      if (med && gd.h1[stage] == kTallBM)
         dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                 gd.row0[1] + ri * kTallBM);
+                                                                 gd.row1[stage] + ri * kTallBM);
       else if (med)
         dl_tile<GATED, FP8, kMedBM, kMedBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                 gd.row0[1] + ri * kMedBM);
+                                                                 gd.row1[stage] + ri * kMedBM);
       else
         dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                     gd.row0[2] + ri * kSmallBM);
+                                                                     gd.row2[stage] + ri * kSmallBM);
     }
   }
   if (probe) {
@@ -523,8 +523,8 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(const FfnParams p) {
     const GroupDesc gd = p.groups[g];
     const WeightDesc wd = p.wtab[g];
     const int local = tile - t0s[g];
-    const int nti = local / gd.nrt[0];
-    const int m0 = (local - nti * gd.nrt[0]) * BM;
+    const int nti = local / gd.nrt[GATED ? 0 : 1][0];
+    const int m0 = (local - nti * gd.nrt[GATED ? 0 : 1][0]) * BM;
     const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
     const int lr = tid >> 2, lk = (tid & 3) * 4;
     const float* asrc = A + (int64_t)(arow0 + min(m0 + lr, gd.n - 1)) * K + lk;

@@ -83,52 +83,66 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
                                                             float* __restrict__ posw) {
   const int tid = threadIdx.x;
   if (blockIdx.x == 0) {
-    __shared__ int32_t wsum2[kPlanThreads / 64 + 1][2];
+    __shared__ int32_t wsum4[kPlanThreads / 64 + 1][4];
     __shared__ int32_t wsum7[kPlanThreads / 64 + 1][7];
     const int G = E + S;
     const int g = tid;
     const bool real = g < G;
     const int n = !real ? 0 : g < E ? (only_expert < 0 || g == only_expert ? depth[g] : 0) : n_tokens;
     const int full = n / big_bm, r = n - full * big_bm;
-    // routed rows, and the full big gate/up tiles of the whole batch
-    int a[2] = {g < E ? n : 0, full * nt.v[0]};
-    int sum2[2];
-    plan_block_scan<2>(a, sum2, wsum2);
-    const int N = sum2[0];
+    // routed rows; full big gate/up tiles of the whole batch; big row tiles
+    // when a remainder above 3/4 of a big tile takes one more (rule A) and
+    // when any remainder above one medium tile does (rule B)
+    int a[4] = {g < E ? n : 0, full * nt.v[0], full + (r > big_bm - big_bm / 4 ? 1 : 0),
+                full + (r > med_bm ? 1 : 0)};
+    int sum4[4];
+    plan_block_scan<4>(a, sum4, wsum4);
+    const int N = sum4[0];
     // A batch whose full big tiles do not fill one round of the grid is
     // cold: its remainders go to medium tiles only (a few long big tiles
     // would be the critical path of a weight-streaming launch).
-    const bool cold = sum2[1] < num_cu;
-    int nrt[3] = {0, 0, 0};
-    int fam1_rows = 0;  // rows covered by family 1 before the small tile
-    int h1 = med_bm;    // rows per family-1 tile
-    if (small_bm == 0) {
-      nrt[0] = (n + big_bm - 1) / big_bm;
-    } else if (cold && r > med_bm) {
-      // full big tiles; a remainder above one medium tile takes one tall
-      // tile (kTallBM rows: the expert's weights are read once)
-      nrt[0] = full;
-      nrt[1] = 1;
-      h1 = kTallBM;
-    } else if (r > big_bm - big_bm / 4) {
-      // a remainder filling more than 3/4 of a big tile takes one more
-      nrt[0] = full + 1;
-    } else {
-      // full big tiles, then full medium tiles; what is left goes to one
-      // more medium tile above small_bm rows, else to one small tile
-      nrt[0] = full;
-      nrt[1] = r / med_bm;
-      const int rem = r - nrt[1] * med_bm;
-      if (rem > small_bm)
-        nrt[1] += 1;
-      else if (rem > 0)
-        nrt[2] = 1;
-      fam1_rows = (r / med_bm) * med_bm;
+    const bool cold = sum4[1] < num_cu;
+    int nrt[2][3] = {{0, 0, 0}, {0, 0, 0}};
+    int fam1_rows[2] = {0, 0};   // rows covered by family 1 before the small tile
+    int h1[2] = {med_bm, med_bm};  // rows per family-1 tile
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      // Rule B trades the medium and small tiles of a remainder (each
+      // streams the expert's weights again, and their per-tile overheads
+      // weigh more) for one big tile with idle rows; it is taken unless its
+      // extra big tiles start another round of the grid in a stage that has
+      // few rounds (there a round of long big tiles would run nearly alone).
+      const int ntb = nt.v[3 * st];
+      const int rounds_a = (sum4[2] * ntb + num_cu - 1) / num_cu;
+      const int rounds_b = (sum4[3] * ntb + num_cu - 1) / num_cu;
+      const int xbig = rounds_b == rounds_a || rounds_a >= 4 ? med_bm : big_bm - big_bm / 4;
+      if (small_bm == 0) {
+        nrt[st][0] = (n + big_bm - 1) / big_bm;
+      } else if (cold && r > med_bm) {
+        // full big tiles; a remainder above one medium tile takes one tall
+        // tile (kTallBM rows: the expert's weights are read once)
+        nrt[st][0] = full;
+        nrt[st][1] = 1;
+        h1[st] = kTallBM;
+      } else if (r > xbig) {
+        nrt[st][0] = full + 1;
+      } else {
+        // full big tiles, then full medium tiles; what is left goes to one
+        // more medium tile above small_bm rows, else to one small tile
+        nrt[st][0] = full;
+        nrt[st][1] = r / med_bm;
+        const int rem = r - nrt[st][1] * med_bm;
+        if (rem > small_bm)
+          nrt[st][1] += 1;
+        else if (rem > 0)
+          nrt[st][2] = 1;
+        fam1_rows[st] = (r / med_bm) * med_bm;
+      }
     }
     int b[7];
     b[0] = n;
 #pragma unroll
-    for (int i = 0; i < 6; ++i) b[1 + i] = nrt[i % 3] * nt.v[i];
+    for (int i = 0; i < 6; ++i) b[1 + i] = nrt[i / 3][i % 3] * nt.v[i];
     int sum7[7];
     plan_block_scan<7>(b, sum7, wsum7);
     if (real) {
@@ -136,14 +150,17 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
       gd.n = n;
       gd.x_row0 = g < E ? b[0] : N;
       gd.y_row0 = b[0];
-      gd.row0[0] = 0;
-      gd.row0[1] = full * big_bm;
-      gd.row0[2] = full * big_bm + fam1_rows;
-#pragma unroll
-      for (int f = 0; f < 3; ++f) gd.nrt[f] = nrt[f];
 #pragma unroll
       for (int i = 0; i < 6; ++i) gd.t0[i] = b[1 + i];
-      gd.h1 = h1;
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int f = 0; f < 3; ++f) gd.nrt[st][f] = nrt[st][f];
+        gd.row1[st] = full * big_bm;
+        gd.row2[st] = full * big_bm + fam1_rows[st];
+        gd.h1[st] = h1[st];
+      }
+      gd.pad[0] = gd.pad[1] = gd.pad[2] = 0;
       groups[g] = gd;
       counts[g] = n;
       offsets[g] = b[0];

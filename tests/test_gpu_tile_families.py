@@ -3,10 +3,14 @@ queue depths (rows mode), against the oracle element by element.
 
 Cold batch (its full 256-row tiles do not fill one round of the grid): a
 remainder above 128 rows takes one tall 256-row tile, 65..128 rows one medium
-tile, 1..64 rows one small tile.  Warm batch: a remainder above 192 rows takes
-one more big tile, otherwise medium tiles and at most one small tile.  The
-depths below put at least one expert on each branch (and exact multiples of
-256, and empty experts), for bf16 and fp8 weights."""
+tile, 1..64 rows one small tile.  Warm batch, per FFN stage: a remainder
+above 128 rows takes one more big tile (rule B), unless those extra big
+tiles would start another round of the grid in a stage with fewer than 4
+rounds; then only a remainder above 192 rows does (rule A) and the others
+take medium tiles and at most one small tile.  The depths below put at least
+one expert on each branch (and exact multiples of 256, and empty experts),
+for bf16 and fp8 weights; the mixed batch splits the same remainder
+differently in its two stages."""
 
 import dataclasses
 
@@ -21,8 +25,14 @@ from gpu_helpers import BF16_RTOL, assert_close, log, make_context, to_dev, to_h
 pytestmark = pytest.mark.gpu
 
 COLD = [300, 200, 100, 40, 1, 256, 0, 129]          # big+small, tall, medium, small, small, big, -, tall
-WARM = [2100, 230, 150, 300, 260, 0, 512, 193]       # 8 big+small, big, medium+small, big+small, big+small,
-                                                     # -, 2 big, big
+# rule B in both stages: 8 big + small, big, big, big + small, big + small, -,
+# 2 big, big, medium
+WARM = [2100, 230, 150, 300, 260, 0, 512, 193, 100]
+# d = 512, f = 896: 128 big row tiles under rule A, 129 under rule B.  Gate/up
+# (7 big column tiles) has 4 rounds either way: rule B, so the 150-row
+# remainder takes a big tile.  Down (2 big column tiles) would go from 1 round
+# to 2: rule A, so that remainder takes a medium and a small tile.
+MIXED = [2048] * 13 + [2198, 2148, 2088]
 
 
 def _rows(w, depths, seed):
@@ -38,15 +48,16 @@ def _rows(w, depths, seed):
     return N, per
 
 
-@pytest.mark.parametrize("kind,wdt", [("cold", "bf16"), ("cold", "fp8"), ("warm", "bf16"), ("warm", "fp8")])
+@pytest.mark.parametrize("kind,wdt", [("cold", "bf16"), ("cold", "fp8"), ("warm", "bf16"), ("warm", "fp8"),
+                                      ("mixed", "bf16")])
 def test_tile_families_match_oracle(kind, wdt):
-    depths = COLD if kind == "cold" else WARM
+    depths = {"cold": COLD, "warm": WARM, "mixed": MIXED}[kind]
     # warm: f = 8192 gives 64 big gate/up column tiles, so 8 + 2 + 1 + 1 + 1
     # full 256-row blocks fill more than one round of 256 CUs
-    f = 320 if kind == "cold" else 8192
-    w = synth.Workload(f"fam_{kind}_{wdt}", 110, d=256, f=f, E=len(depths), k=1, zipf_s=1.0, mode="rows",
+    d, f = {"cold": (256, 320), "warm": (256, 8192), "mixed": (512, 896)}[kind]
+    w = synth.Workload(f"fam_{kind}_{wdt}", 110, d=d, f=f, E=len(depths), k=1, zipf_s=1.0, mode="rows",
                        depth_max=max(depths), wdt=wdt)
-    N, per = _rows(w, depths, 11 if kind == "cold" else 12)
+    N, per = _rows(w, depths, {"cold": 11, "warm": 12, "mixed": 13}[kind])
     log(f"case {kind}/{wdt}: depths {depths}, d={w.d} f={w.f}")
     ws = synth.all_expert_weights(w, 0, threads=4)
     ctx = make_context(w, max_tokens=N)
