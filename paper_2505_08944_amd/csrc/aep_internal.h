@@ -32,18 +32,19 @@ struct WeightDesc {
 static_assert(sizeof(WeightDesc) == 48, "WeightDesc layout");
 
 // One FFN group of a drained batch, written by the plan kernel.  A group's
-// rows are covered by up to three row-tile families (bf16 / fp8 weights):
-// "big" 256-row tiles over the full 256-row blocks (plus one more when the
-// remainder exceeds 192 rows, unless the batch is cold), then "medium"
-// 128-row tiles and at most one "small" 64-row tile over the remainder.  In
-// a cold batch a remainder above 128 rows takes one "tall" 256-row tile
-// (kTallBM) in family 1 instead (h1 = kTallBM), so a cold expert's weights
-// are streamed once.  f32 weights use the big family alone, with 64-row
-// tiles.  Family f covers rows [row0[f], row0[f] + nrt[f] * height), clamped
-// to n (family 1 height: h1).  t0[stage * 3 + f] is the group's first tile id
-// in family f of a stage (0: gate/up, 1: down).
-// Row tiles of one group, per FFN stage (0: gate/up, 1: down): the two
-// stages may split a group's remainder rows differently.
+// rows are covered by up to three row-tile families (bf16 / fp8 weights),
+// chosen per FFN stage (0: gate/up, 1: down): "big" 256-row tiles over the
+// full 256-row blocks, plus one more for a remainder above 128 rows (above
+// 192 rows in a stage where the extra big tiles would start another round
+// of the grid and that has fewer than 4 rounds; never in a cold batch), then
+// "medium" 128-row tiles and at most one "small" 64-row tile over the
+// remainder.  In a cold batch a remainder above 128 rows takes one "tall"
+// 256-row tile (kTallBM) in family 1 instead (h1 = kTallBM), so a cold
+// expert's weights are streamed once.  f32 weights use the big family alone,
+// with 64-row tiles.  In stage s, family 0 covers rows [0, nrt[s][0] * 256),
+// family 1 [row1[s], row1[s] + nrt[s][1] * h1[s]) and family 2 [row2[s],
+// row2[s] + nrt[s][2] * 64), clamped to n.  t0[s * 3 + f] is the group's first
+// tile id in family f of stage s.
 struct GroupDesc {
   int32_t n;          // rows
   int32_t x_row0;     // first row in x_perm

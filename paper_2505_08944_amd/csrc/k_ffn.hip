@@ -4,16 +4,20 @@
 //   gate/up:  h[r, c] = silu(x_r . W_gate[c]) * (x_r . W_up[c])   (K = d)
 //   down:     y[r, c] = h_r . W_down[c]                            (K = f)
 //
-// The plan kernel laid the tiles of all groups (experts) end to end in two
-// families: 256 x 256 tiles for the full row blocks of hot experts, and
-// 64 x 128 tiles for cold experts and the ragged row tails of hot ones.  One
+// The plan kernel laid the tiles of all groups (experts) end to end in three
+// row-tile families, split per stage: 256 x 256 tiles for the full 256-row
+// blocks of an expert (and for a remainder above 128 rows, unless that would
+// start another round of the grid in a short stage), then 128 x 128 medium
+// tiles (256 x 128 tall ones for a cold batch's remainders above 128 rows)
+// and 64 x 128 small tiles for the ragged row tails and cold experts.  One
 // launch covers a whole skewed batch, from a 1-row expert to the hottest one:
-// every big tile first, then the small ones, which also fill the tail of the
-// big family.  The workgroup -> tile map is XCD aware: hardware dispatches
-// workgroups round robin over the 8 XCDs, so workgroup w works on slot
-// (w % 8) * (grid / 8) + w / 8, giving each XCD (and its L2) a contiguous run
-// of tiles, and the big tiles of a group are ordered in panels of 8 column
-// tiles so that such a run is a compact block of row and column tiles.
+// every big tile first, then the smaller ones, which also fill the tail of
+// the big family.  The workgroup -> tile map is XCD aware: hardware
+// dispatches workgroups round robin over the 8 XCDs, so workgroup w works on
+// slot (w % 8) * (grid / 8) + w / 8, giving each XCD (and its L2) a
+// contiguous run of tiles, and the big tiles of a group are ordered in panels
+// of 8 column tiles so that such a run is a compact block of row and column
+// tiles.
 //
 // bf16 / fp8-weight path: 256-thread workgroups, K step 64, four waves each
 // owning a quadrant of the tile computed with v_mfma_f32_32x32x16_bf16 (f32
@@ -460,8 +464,8 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 // The FFN launch for bf16 or fp8 weights: every tile of the big family (256
 // rows), then the medium (128 rows; 256 for a cold expert's remainder above
 // 128 rows) and small (64 rows) tiles of the row remainders and of cold
-// experts, in one persistent grid.  The smaller
-// families come last, so they also fill the tail of the big one; cold
+// experts, in one persistent grid.  The smaller families come last, so they
+// also fill the tail of the big one; cold
 // experts are weight-streaming bound, and narrow tiles spread each expert's
 // weights over more CUs.  fp8 stages are smaller (e4m3 B tiles), so the rings
 // are deeper: 3 big / 6 medium and small stages instead of 2 / 4.
