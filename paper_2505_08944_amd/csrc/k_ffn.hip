@@ -170,7 +170,12 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   static_assert(BM * kLd * 2 <= CAP, "epilogue staging must fit");
   static_assert((STAGES - 1) * kPerStep < 64, "vmcnt range");
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The thread index goes through an empty asm so that the per-lane offsets
+  // derived from it are computed per tile instead of being hoisted out of the
+  // tile loop, where they would stay live across the K loop and be spilled.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int K = p.K, KT = K / BKS, n_out = p.n_out;
   const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
