@@ -61,19 +61,22 @@ __device__ __forceinline__ int c_row(int lane, int r) {
 }
 
 // Tile order inside one group's nrow x ncol grid of big tiles: panels of
-// kPanel column tiles, row tiles one after another inside a panel, the
+// PANEL column tiles, row tiles one after another inside a panel, the
 // columns of a row tile adjacent.  The persistent grids hand each XCD runs of
-// consecutive tile ids (32 for 256 workgroups), so an XCD works on a 4 x 8
-// block of tiles: per K step its L2 sees 4 row bands of A and 8 column bands
-// of B instead of every row band of the group against one column band.
-constexpr int kPanel = 8;
+// consecutive tile ids (32 for 256 workgroups), so an XCD works on a compact
+// block of tiles (4 x 8 for gate/up, 8 x 4 for down): per K step its L2 sees
+// a few row bands of A and column bands of B instead of every row band of the
+// group against one column band.  Down launches have few column tiles
+// (d / 256) and long K; panels of 4 measured 1-4% faster there, panels of 8
+// faster for gate/up on single experts.
+template <int PANEL>
 __device__ __forceinline__ void panel_decode(int local, int nrow, int ncol, int& rt, int& ct) {
-  const int per = kPanel * nrow;
+  const int per = PANEL * nrow;
   const int pi = local / per;
   const int within = local - pi * per;
-  const int w = min(kPanel, ncol - pi * kPanel);  // the last panel may be narrower
+  const int w = min(PANEL, ncol - pi * PANEL);  // the last panel may be narrower
   rt = within / w;
-  ct = pi * kPanel + (within - rt * w);
+  ct = pi * PANEL + (within - rt * w);
 }
 
 __device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
@@ -516,7 +519,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const GroupDesc gd = p.groups[g];
       const int local = tile - t0f[0][g];
       int rt, nti;
-      panel_decode(local, gd.nrt[stage][0], ncol_big, rt, nti);
+      panel_decode<GATED ? 8 : 4>(local, gd.nrt[stage][0], ncol_big, rt, nti);
       dl_tile<GATED, FP8, kBM, kBN, kBigStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
     } else {
       // medium or small: the row tiles of one column tile are consecutive
