@@ -106,7 +106,10 @@ typedef struct {
 const char* aep_status_string(aep_status s);
 
 /* Create a context for cfg (copied).  Validates the configuration; allocates
- * host state only.  *out receives the handle.  No device work. */
+ * host state only.  *out receives the handle.  No device work.
+ * AEP_ERR_UNSUPPORTED for a shape the kernels do not cover (d or f not a
+ * multiple of 64; with BF16 activations, 2 * d * f bytes, or
+ * 2 * max_tokens_per_layer * max(d, f) bytes, of 4 GiB or more). */
 aep_status aep_create(const aep_config* cfg, void** out);
 
 /* Destroy a context (NULL is allowed).  Does not free the caller's workspace. */

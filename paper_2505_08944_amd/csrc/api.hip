@@ -192,6 +192,15 @@ aep_status aep_create(const aep_config* cfg, void** out) {
     const bool known = (g.act_dtype >= 0 && g.act_dtype <= 2) && (g.w_dtype >= 0 && g.w_dtype <= 2);
     return known ? AEP_ERR_UNSUPPORTED : AEP_ERR_INVALID_ARG;
   }
+  // The bf16 / fp8 FFN kernels address one group's activation rows (at most
+  // max_tokens_per_layer rows of d or f elements) and one weight matrix
+  // through buffer resources: 32-bit byte offsets and sizes.
+  if (bf) {
+    const uint64_t lim = 1ull << 32;
+    const uint64_t kmax = (uint64_t)std::max(g.d_model, g.d_ffn);
+    if ((uint64_t)g.max_tokens_per_layer * kmax * 2 >= lim || (uint64_t)g.d_model * g.d_ffn * 2 >= lim)
+      return AEP_ERR_UNSUPPORTED;
+  }
   Ctx* c = new (std::nothrow) Ctx();
   if (!c) return AEP_ERR_CAPACITY;
   c->cfg = g;

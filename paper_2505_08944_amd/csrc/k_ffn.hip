@@ -92,8 +92,9 @@ __device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
 }
 
 // ------------------------------------------------- direct-to-LDS MFMA tiles
-// Tiles move from global memory straight into LDS (global_load_lds_dwordx4:
-// 64 lanes x 16 bytes into 1 KB of consecutive LDS, no staging registers),
+// Tiles move from global memory straight into LDS (buffer_load_dwordx4 with
+// the lds bit: 64 lanes x 16 bytes into 1 KB of consecutive LDS, no staging
+// registers),
 // through a ring of STAGES LDS buffers with a prefetch distance of
 // STAGES - 1 K steps.  LDS rows are not padded; a 16-byte chunk c of tile row r sits at position
 // c ^ s(r), where s spreads the 8 rows read together by one fragment read
@@ -103,14 +104,30 @@ __device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
 typedef __attribute__((address_space(3))) void* lds_vptr;
 typedef const __attribute__((address_space(1))) void* glb_vptr;
 
-// One direct global -> LDS load: 64 lanes x 16 bytes to lds_addr + 16 * lane.
-// Issued through inline asm so that the compiler does not see an LDS write
-// it cannot disambiguate (it would otherwise wait for every outstanding load
-// before each LDS read); the kernel orders these loads itself with
-// wait_vmcnt + barriers.  M0 holds the LDS destination.
-__device__ __forceinline__ void dload16(const void* gptr, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr),
-               "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+// A raw buffer resource over [base, base + bytes): stride 0, 32-bit data
+// format, every access bounds-checked against bytes (an access past the end
+// reads zeros and writes nothing).  The fields are uniform (SGPRs).
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  i32x4_t r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xFFFFu));
+  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+  r.w = 0x00020000;  // data format 32
+  return r;
+}
+
+// One direct buffer -> LDS load: lane l reads the 16 bytes at byte offset
+// voff + soff of the resource and writes them to lds_addr + 16 * l (M0 holds
+// lds_addr).  The per-step K offset rides in the scalar soff, so a load costs
+// no vector address arithmetic.  Issued through inline asm so that the
+// compiler does not see an LDS write it cannot disambiguate (it would
+// otherwise wait for every outstanding load before each LDS read); the
+// kernel orders these loads itself with wait_vmcnt + barriers.
+__device__ __forceinline__ void dload16(i32x4_t rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc),
+               "s"(soff), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
                : "memory", "m0");
 }
 
@@ -205,13 +222,16 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // group's end are not loaded (their LDS rows hold stale data, their outputs
   // are never stored), which saves the activation traffic of ragged and cold
   // tiles.  Every K step of the tile issues the same number of loads per wave.
-  const int na_eff = __builtin_amdgcn_readfirstlane(
+  // Big bf16 tiles (two-stage ring) load every block: rows past the end
+  // repeat the last row, and the refill carries no per-load branches.
+  constexpr bool kAllA = !FP8 && STAGES == 2;
+  const int na_eff = kAllA ? kNA : __builtin_amdgcn_readfirstlane(
       max(0, min(kNA, (alast + 1 - wave * kNA * kRplA + kRplA - 1) / kRplA)));
   const int per_step = na_eff + kNB;
-  uint32_t aoff[kNA], boff[kNB];
+  uint32_t aoff[kNA], boff[kNB];  // byte offsets into the two resources
 #pragma unroll
   for (int i = 0; i < kNA; ++i)
-    aoff[i] = (uint32_t)(min((wave * kNA + i) * kRplA + lda_row, alast) * K + lda_c * 8);
+    aoff[i] = (uint32_t)(min((wave * kNA + i) * kRplA + lda_row, alast) * K + lda_c * 8) * 2u;
   // B rows: a wave column's TN rows are TN/2 gate features then the same TN/2
   // up features; a wave's B rows lie in one of the two halves.
   const unsigned char* bmat;
@@ -220,12 +240,16 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     const bool up = GATED && (br0 % TN) >= TN / 2;
     bmat = reinterpret_cast<const unsigned char*>(GATED ? (up ? wd.up : wd.gate) : wd.down);
   }
+  // the group's rows from row m0 on, and the weight matrix (the host bounds
+  // both below 4 GiB)
+  const i32x4_t rsA = make_rsrc(abase, (uint32_t)(alast + 1) * (uint32_t)K * 2u);
+  const i32x4_t rsB = make_rsrc(bmat, (uint32_t)n_out * (uint32_t)K * (FP8 ? 1u : 2u));
 #pragma unroll
   for (int i = 0; i < kNB; ++i) {
     const int br = (wave * kNB + i) * kRplB + ldb_row;
     int c = GATED ? nti * (BN / 2) + (br / TN) * (TN / 2) + (br % TN) % (TN / 2) : nti * BN + br;
     c = min(c, n_out - 1);
-    boff[i] = (uint32_t)(c * K * (FP8 ? 1 : 2) + ldb_c * 16);  // bytes
+    boff[i] = (uint32_t)(c * K * (FP8 ? 1 : 2) + ldb_c * 16);
   }
 
 #define DL_LOAD(kt_, st_)                                                                        \
@@ -233,9 +257,9 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     const uint32_t sa_ = lds_base + (st_) * kStageB + wave * kNA * 1024;                          \
     const uint32_t sb_ = lds_base + (st_) * kStageB + kTileA + wave * kNB * 1024;                 \
     _Pragma("unroll") for (int i = 0; i < kNA; ++i)                                              \
-        if (i < na_eff) dload16(abase + aoff[i] + (kt_) * BKS, sa_ + i * 1024);                  \
+        if (i < na_eff) dload16(rsA, aoff[i], (kt_) * kRowA, sa_ + i * 1024);                    \
     _Pragma("unroll") for (int i = 0; i < kNB; ++i)                                              \
-        dload16(bmat + boff[i] + (kt_) * kRowB, sb_ + i * 1024);                                 \
+        dload16(rsB, boff[i], (kt_) * kRowB, sb_ + i * 1024);                                    \
   } while (0)
   // bf16 weights: k-slice ks (16 k) of every fragment
 #define DL_READ(st_, ks_, A_, B_)                                                                \
@@ -305,35 +329,44 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     __builtin_amdgcn_sched_barrier(0);                                                           \
   } while (0)
 
-  // Two-stage rings (bf16 big tiles): the refill after the barrier that
-  // frees a stage goes out between the MFMA rows of the next operand group
-  // (row q, NI MFMAs, is followed by A loads q * kNA / MI .. and B loads
-  // q * kNB / MI ..).  Issued as one block, the loads stall every wave at
-  // issue until the address unit has taken them, while its matrix pipe runs
-  // dry (the interleaved refill: down launches -5..-9%, gate/up -1..-4%).
-  // Deeper rings (fp8 big tiles, the smaller families) keep the block, which
-  // measured faster there.
-#define DL_GROUP_L(st_, An, Bn, Ac, Bc, LK, LST)                                                 \
+  // Two-stage rings (bf16 big tiles): the refill of the stage freed by a
+  // barrier (kNA + kNB loads per wave, listed A block 0, B block 0, A block
+  // 1, ...) goes out one load after every second MFMA of the 32 MFMAs that
+  // follow the barrier, i.e. over the first two operand groups of the step.
+  // Loads bunched after the barrier queue up at the address unit (four waves
+  // issue theirs at once) and stall the issuing wave, and with it its matrix
+  // pipe; spread this way they leave 32 MFMAs for the last load to land.
+  // The group's own operand reads (next slice) go out one per MFMA over its
+  // first MI + NI MFMAs.  Deeper rings (fp8 big tiles, the smaller families)
+  // issue their refill as one block, which measured faster there.
+  // GB: index of the group's first MFMA counted from the barrier.
+#define DL_READ1(st_, ks_, A_, B_, idx_)                                                         \
   do {                                                                                           \
-    static_assert(kNA % MI == 0 && kNB % MI == 0, "loads per MFMA row");                         \
+    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
+    const int ro_ = rd_row * kRowA + (((2 * (ks_) + (lane >> 5)) ^ rd_sa) << 4);                 \
+    if ((idx_) < MI)                                                                             \
+      A_[(idx_)] = *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + (idx_) * 32) * kRowA + ro_); \
+    else                                                                                         \
+      B_[(idx_) - MI] = *reinterpret_cast<const bf16x8_t*>(                                      \
+          ab_ + kTileA + (wn * TN + ((idx_) - MI) * 32) * kRowB + ro_);                          \
+  } while (0)
+#define DL_GROUP_R(st_, ks_, An, Bn, Ac, Bc, LK, LST, GB)                                        \
+  do {                                                                                           \
+    static_assert(kNA == kNB && kNA + kNB == MI * NI, "one load per two MFMAs of two groups"); \
     const uint32_t sa_ = lds_base + (LST) * kStageB + wave * kNA * 1024;                          \
     const uint32_t sb_ = lds_base + (LST) * kStageB + kTileA + wave * kNB * 1024;                 \
-    DL_READ(st_, 0, An, Bn);                                                                     \
-    _Pragma("unroll") for (int q_ = 0; q_ < MI; ++q_) {                                          \
-      _Pragma("unroll") for (int j_ = 0; j_ < NI; ++j_) acc[q_][j_] =                            \
-          __builtin_amdgcn_mfma_f32_32x32x16_bf16(Ac[q_], Bc[j_], acc[q_][j_], 0, 0, 0);        \
-      if (q_ == 0) {                                                                             \
-        __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);                                 \
-        __builtin_amdgcn_sched_group_barrier(0x008, NI, 0);                                      \
-      }                                                                                          \
+    _Pragma("unroll") for (int m_ = 0; m_ < MI * NI; ++m_) {                                     \
+      if (m_ < MI + NI) DL_READ1(st_, ks_, An, Bn, m_);                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
-      _Pragma("unroll") for (int r_ = 0; r_ < kNA / MI; ++r_) {                                  \
-        const int i_ = q_ * (kNA / MI) + r_;                                                     \
-        if (i_ < na_eff) dload16(abase + aoff[i_] + (LK) * BKS, sa_ + i_ * 1024);               \
-      }                                                                                          \
-      _Pragma("unroll") for (int r_ = 0; r_ < kNB / MI; ++r_) {                                  \
-        const int i_ = q_ * (kNB / MI) + r_;                                                     \
-        dload16(bmat + boff[i_] + (LK) * kRowB, sb_ + i_ * 1024);                                \
+      acc[m_ / NI][m_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                           \
+          Ac[m_ / NI], Bc[m_ % NI], acc[m_ / NI][m_ % NI], 0, 0, 0);                             \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      if (m_ % 2 == 1) {                                                                         \
+        const int l_ = ((GB) + m_) / 2;                                                          \
+        if (l_ % 2 == 0)                                                                         \
+          dload16(rsA, aoff[l_ / 2], (LK) * kRowA, sa_ + (l_ / 2) * 1024);                       \
+        else                                                                                     \
+          dload16(rsB, boff[l_ / 2], (LK) * kRowB, sb_ + (l_ / 2) * 1024);                       \
       }                                                                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \
@@ -361,7 +394,29 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // is refilled with step kt + STAGES: a step's loads have STAGES - 1 whole
   // steps of MFMA work to land.  Past the last step the loads repeat the
   // last step (never read).
-  if constexpr (!FP8) {
+  if constexpr (!FP8 && STAGES == 2) {
+    // The refill of step kt + 2 into stage st starts after the barrier that
+    // ends step kt (in the group computing its last slice) and ends in the
+    // first group of step kt + 1.  That group's first pass repeats half of
+    // the prologue's loads of step 1 (same bytes, same place; they land
+    // before the barrier that ends step 0).
+    bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
+    DL_READ(0, 0, a0, b0);
+    int st = 0;
+    int lk = min(1, KT - 1), lst = 1;  // the refill in flight: its step and stage
+    for (int kt = 0; kt < KT; ++kt) {
+      const int nst = st ^ 1;
+      DL_GROUP_R(st, 1, a1, b1, a0, b0, lk, lst, MI * NI);
+      DL_GROUP(st, 2, a0, b0, a1, b1);
+      DL_GROUP(st, 3, a1, b1, a0, b0);
+      wait_vmcnt<0>();  // step kt + 1 has landed (this wave's part)
+      __syncthreads();  // ... and every wave's; stage st is free
+      lk = min(kt + STAGES, KT - 1);
+      lst = st;
+      DL_GROUP_R(nst, 0, a0, b0, a1, b1, lk, lst, 0);
+      st = nst;
+    }
+  } else if constexpr (!FP8) {
     bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
     DL_READ(0, 0, a0, b0);
     int st = 0;
@@ -372,13 +427,9 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       DL_GROUP(st, 3, a1, b1, a0, b0);
       wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
-      if constexpr (STAGES == 2) {
-        DL_GROUP_L(nst, a0, b0, a1, b1, min(kt + STAGES, KT - 1), st);
-      } else {
-        DL_LOAD(min(kt + STAGES, KT - 1), st);
-        __builtin_amdgcn_sched_barrier(0);
-        DL_GROUP(nst, 0, a0, b0, a1, b1);
-      }
+      DL_LOAD(min(kt + STAGES, KT - 1), st);
+      __builtin_amdgcn_sched_barrier(0);
+      DL_GROUP(nst, 0, a0, b0, a1, b1);
       st = nst;
     }
   } else {
@@ -397,7 +448,8 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       st = nst;
     }
   }
-#undef DL_GROUP_L
+#undef DL_GROUP_R
+#undef DL_READ1
 #undef DL_GROUP8
 #undef DL_GROUP
 #undef DL_MMA

@@ -59,12 +59,26 @@ def test_status_strings():
     (dict(max_tokens_per_layer=1 << 24), 1), (dict(d_model=100), 6), (dict(d_ffn=96), 6),
     (dict(act_dtype=0, w_dtype=1), 6), (dict(act_dtype=1, w_dtype=0), 6), (dict(act_dtype=2), 6),
     (dict(act_dtype=7), 1), (dict(n_experts=1000, n_shared=30), 1),
+    # bf16 / fp8 kernels: 32-bit byte offsets into a weight matrix and a group's rows
+    (dict(d_model=65536, d_ffn=32768), 6), (dict(d_model=32768, d_ffn=65536, w_dtype=2), 6),
+    (dict(max_tokens_per_layer=1 << 22), 6),
 ])
 def test_create_rejects_bad_configs(kw, status):
     L, lib = _lib()
     st, h = _create(L, lib, **kw)
     assert st == status, (kw, st)
     assert not h.value
+
+
+@pytest.mark.parametrize("kw", [
+    dict(d_model=65536, d_ffn=32704), dict(max_tokens_per_layer=(1 << 22) - 1),
+    dict(d_model=65536, d_ffn=32768, act_dtype=0, w_dtype=0),  # f32 kernels: no such bound
+])
+def test_create_accepts_sizes_below_the_offset_bound(kw):
+    L, lib = _lib()
+    st, h = _create(L, lib, **kw)
+    assert st == 0, (kw, st)
+    assert lib.aep_destroy(h) == 0
 
 
 def test_workspace_accounting_and_unbound_state():
