@@ -313,20 +313,57 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
   } while (0)
-  // fp8: widen the raw B read in the previous group, then read the next
-  // half-step while the MFMAs of this one run
-#define DL_GROUP8(st_, m_, A1n, A2n, Rn, A1c, A2c, Rc)                                           \
+  // fp8: one operand fragment of half-step m (index < NI: raw B, then A1, A2)
+#define DL_READ8_1(st_, m_, A1_, A2_, R_, idx_)                                                  \
   do {                                                                                           \
+    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
+    const int ca_ = 4 * (m_) + 2 * (lane >> 5);                                                  \
+    if ((idx_) < NI) {                                                                           \
+      const int rb_ = rd_row * kRowB + (((2 * (m_) + (lane >> 5)) ^ rd_sb) << 4);                \
+      R_[(idx_)] = *reinterpret_cast<const uint4*>(ab_ + kTileA + (wn * TN + (idx_) * 32) * kRowB + rb_); \
+    } else if ((idx_) < NI + MI) {                                                               \
+      const int ra1_ = rd_row * kRowA + ((ca_ ^ rd_sa) << 4);                                    \
+      A1_[(idx_) - NI] = *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + ((idx_) - NI) * 32) * kRowA + ra1_); \
+    } else {                                                                                     \
+      const int ra2_ = rd_row * kRowA + (((ca_ + 1) ^ rd_sa) << 4);                              \
+      A2_[(idx_) - NI - MI] = *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + ((idx_) - NI - MI) * 32) * kRowA + ra2_); \
+    }                                                                                            \
+  } while (0)
+  // fp8: widen the raw B read in the previous group, then read the next
+  // half-step while the 2 * MI * NI MFMAs of this one run; the refill is
+  // spread over the step's MFMAs as in the deeper bf16 rings (DL_GROUP_S).
+#define DL_GROUP8_S(st_, m_, A1n, A2n, Rn, A1c, A2c, Rc, LK, LST, GB)                             \
+  do {                                                                                           \
+    constexpr int MN_ = MI * NI, M2_ = 2 * MI * NI, MT_ = 4 * MI * NI, LT_ = kNA + kNB,          \
+                  R_ = 2 * MI + NI;                                                              \
+    const uint32_t sa_ = lds_base + (LST) * kStageB + wave * kNA * 1024;                          \
+    const uint32_t sb_ = lds_base + (LST) * kStageB + kTileA + wave * kNB * 1024;                 \
     DL_WIDEN(Rc, b1, b2);                                                                        \
     __builtin_amdgcn_sched_barrier(0);                                                           \
-    DL_READ8(st_, m_, A1n, A2n, Rn);                                                             \
-    DL_MMA(A1c, b1);                                                                             \
-    DL_MMA(A2c, b2);                                                                             \
-    _Pragma("unroll") for (int q_ = 0; q_ < 2 * kQ; ++q_) {                                      \
-      __builtin_amdgcn_sched_group_barrier(0x100, (2 * MI + NI + 2 * kQ - 1) / (2 * kQ), 0);     \
-      __builtin_amdgcn_sched_group_barrier(0x008, MI * NI / kQ, 0);                              \
+    _Pragma("unroll") for (int q_ = 0; q_ < M2_; ++q_) {                                         \
+      _Pragma("unroll") for (int r_ = q_ * R_ / M2_; r_ < (q_ + 1) * R_ / M2_; ++r_)             \
+          DL_READ8_1(st_, m_, A1n, A2n, Rn, r_);                                                 \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      if (q_ < MN_)                                                                              \
+        acc[q_ / NI][q_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                         \
+            A1c[q_ / NI], b1[q_ % NI], acc[q_ / NI][q_ % NI], 0, 0, 0);                          \
+      else                                                                                       \
+        acc[(q_ - MN_) / NI][(q_ - MN_) % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(         \
+            A2c[(q_ - MN_) / NI], b2[(q_ - MN_) % NI], acc[(q_ - MN_) / NI][(q_ - MN_) % NI], 0, 0, 0); \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      _Pragma("unroll") for (int l_ = 0; l_ < LT_; ++l_) {                                       \
+        if ((l_ * MT_) / LT_ == (GB) + q_) {                                                     \
+          const bool isa_ = l_ < 2 * kMinAB ? (l_ % 2 == 0) : (kNA > kNB);                       \
+          const int ix_ = l_ < 2 * kMinAB ? l_ / 2 : kMinAB + (l_ - 2 * kMinAB);                 \
+          if (isa_) {                                                                            \
+            if (ix_ < na_eff) dload16(rsA, aoff[ix_], (LK) * kRowA, sa_ + ix_ * 1024);           \
+          } else {                                                                               \
+            dload16(rsB, boff[ix_], (LK) * kRowB, sb_ + ix_ * 1024);                             \
+          }                                                                                      \
+        }                                                                                        \
+      }                                                                                          \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
   } while (0)
 
   // Two-stage rings (bf16 big tiles): the refill of the stage freed by a
@@ -337,9 +374,8 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // issue theirs at once) and stall the issuing wave, and with it its matrix
   // pipe; spread this way they leave 32 MFMAs for the last load to land.
   // The group's own operand reads (next slice) go out one per MFMA over its
-  // first MI + NI MFMAs.  Deeper rings (fp8 big tiles, the smaller families)
-  // issue their refill as one block, which measured faster there.
-  // GB: index of the group's first MFMA counted from the barrier.
+  // first MI + NI MFMAs.  GB: index of the group's first MFMA counted from
+  // the barrier.
 #define DL_READ1(st_, ks_, A_, B_, idx_)                                                         \
   do {                                                                                           \
     const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
@@ -349,6 +385,40 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     else                                                                                         \
       B_[(idx_) - MI] = *reinterpret_cast<const bf16x8_t*>(                                      \
           ab_ + kTileA + (wn * TN + ((idx_) - MI) * 32) * kRowB + ro_);                          \
+  } while (0)
+  // Deeper rings (the medium, small and tall families, fp8 big tiles): the
+  // refill of a freed stage is spread evenly over all MFMAs of the next step
+  // (refill list entry l, A and B blocks alternating while both remain, goes
+  // out after MFMA (l * MT) / LT of the step: MT MFMAs, LT loads), and the
+  // group's operand reads over its MFMAs.  Against one block of loads after
+  // the barrier: EP-share cold experts -10% (bf16 and fp8), fp8 4096-row
+  // expert -6..-11%.
+  constexpr int kMinAB = kNA < kNB ? kNA : kNB;
+#define DL_GROUP_S(st_, ks_, An, Bn, Ac, Bc, LK, LST, GB)                                        \
+  do {                                                                                           \
+    constexpr int MN_ = MI * NI, MT_ = 4 * MI * NI, LT_ = kNA + kNB, R_ = MI + NI;               \
+    const uint32_t sa_ = lds_base + (LST) * kStageB + wave * kNA * 1024;                          \
+    const uint32_t sb_ = lds_base + (LST) * kStageB + kTileA + wave * kNB * 1024;                 \
+    _Pragma("unroll") for (int m_ = 0; m_ < MN_; ++m_) {                                         \
+      _Pragma("unroll") for (int r_ = m_ * R_ / MN_; r_ < (m_ + 1) * R_ / MN_; ++r_)             \
+          DL_READ1(st_, ks_, An, Bn, r_);                                                        \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      acc[m_ / NI][m_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                           \
+          Ac[m_ / NI], Bc[m_ % NI], acc[m_ / NI][m_ % NI], 0, 0, 0);                             \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      _Pragma("unroll") for (int l_ = 0; l_ < LT_; ++l_) {                                       \
+        if ((l_ * MT_) / LT_ == (GB) + m_) {                                                     \
+          const bool isa_ = l_ < 2 * kMinAB ? (l_ % 2 == 0) : (kNA > kNB);                       \
+          const int ix_ = l_ < 2 * kMinAB ? l_ / 2 : kMinAB + (l_ - 2 * kMinAB);                 \
+          if (isa_) {                                                                            \
+            if (ix_ < na_eff) dload16(rsA, aoff[ix_], (LK) * kRowA, sa_ + ix_ * 1024);           \
+          } else {                                                                               \
+            dload16(rsB, boff[ix_], (LK) * kRowB, sb_ + ix_ * 1024);                             \
+          }                                                                                      \
+        }                                                                                        \
+      }                                                                                          \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+    }                                                                                            \
   } while (0)
 #define DL_GROUP_R(st_, ks_, An, Bn, Ac, Bc, LK, LST, GB)                                        \
   do {                                                                                           \
@@ -417,19 +487,24 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       st = nst;
     }
   } else if constexpr (!FP8) {
+    // Deeper rings: the refill of step kt + STAGES into stage st is spread
+    // over the four operand groups of step kt + 1 (it has STAGES - 2 more
+    // steps to land).  The first pass repeats loads of the prologue's last
+    // step (same bytes, same place).
     bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
     DL_READ(0, 0, a0, b0);
     int st = 0;
+    int lk = min(STAGES - 1, KT - 1), lst = STAGES - 1;  // the refill in flight
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st + 1 == STAGES ? 0 : st + 1;
-      DL_GROUP(st, 1, a1, b1, a0, b0);
-      DL_GROUP(st, 2, a0, b0, a1, b1);
-      DL_GROUP(st, 3, a1, b1, a0, b0);
+      DL_GROUP_S(st, 1, a1, b1, a0, b0, lk, lst, MI * NI);
+      DL_GROUP_S(st, 2, a0, b0, a1, b1, lk, lst, 2 * MI * NI);
+      DL_GROUP_S(st, 3, a1, b1, a0, b0, lk, lst, 3 * MI * NI);
       wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
-      DL_LOAD(min(kt + STAGES, KT - 1), st);
-      __builtin_amdgcn_sched_barrier(0);
-      DL_GROUP(nst, 0, a0, b0, a1, b1);
+      lk = min(kt + STAGES, KT - 1);
+      lst = st;
+      DL_GROUP_S(nst, 0, a0, b0, a1, b1, lk, lst, 0);
       st = nst;
     }
   } else {
@@ -437,20 +512,23 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     uint4 r0[NI], r1[NI];
     DL_READ8(0, 0, a10, a20, r0);
     int st = 0;
+    int lk = min(STAGES - 1, KT - 1), lst = STAGES - 1;  // the refill in flight
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st + 1 == STAGES ? 0 : st + 1;
-      DL_GROUP8(st, 1, a11, a21, r1, a10, a20, r0);
+      DL_GROUP8_S(st, 1, a11, a21, r1, a10, a20, r0, lk, lst, 2 * MI * NI);
       wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
-      DL_LOAD(min(kt + STAGES, KT - 1), st);
-      __builtin_amdgcn_sched_barrier(0);
-      DL_GROUP8(nst, 0, a10, a20, r0, a11, a21, r1);
+      lk = min(kt + STAGES, KT - 1);
+      lst = st;
+      DL_GROUP8_S(nst, 0, a10, a20, r0, a11, a21, r1, lk, lst, 0);
       st = nst;
     }
   }
 #undef DL_GROUP_R
+#undef DL_GROUP_S
 #undef DL_READ1
-#undef DL_GROUP8
+#undef DL_GROUP8_S
+#undef DL_READ8_1
 #undef DL_GROUP
 #undef DL_MMA
 #undef DL_WIDEN
