@@ -49,15 +49,20 @@ def _rows(w, depths, seed):
 
 
 @pytest.mark.parametrize("kind,wdt", [("cold", "bf16"), ("cold", "fp8"), ("warm", "bf16"), ("warm", "fp8"),
-                                      ("mixed", "bf16")])
+                                      ("mixed", "bf16"), ("short1", "bf16"), ("short1", "fp8"),
+                                      ("short2", "bf16"), ("short2", "fp8")])
 def test_tile_families_match_oracle(kind, wdt):
-    depths = {"cold": COLD, "warm": WARM, "mixed": MIXED}[kind]
+    # short1 / short2: the cold depths with K of 1, 2 or 3 steps of 64 in the
+    # two stages, fewer than every ring's stages (the first pass of a refill
+    # repeats loads of the prologue; past the last step loads repeat it)
+    depths = {"cold": COLD, "warm": WARM, "mixed": MIXED, "short1": COLD, "short2": COLD}[kind]
     # warm: f = 8192 gives 64 big gate/up column tiles, so 8 + 2 + 1 + 1 + 1
     # full 256-row blocks fill more than one round of 256 CUs
-    d, f = {"cold": (256, 320), "warm": (256, 8192), "mixed": (512, 896)}[kind]
+    d, f = {"cold": (256, 320), "warm": (256, 8192), "mixed": (512, 896), "short1": (64, 192),
+            "short2": (128, 64)}[kind]
     w = synth.Workload(f"fam_{kind}_{wdt}", 110, d=d, f=f, E=len(depths), k=1, zipf_s=1.0, mode="rows",
                        depth_max=max(depths), wdt=wdt)
-    N, per = _rows(w, depths, {"cold": 11, "warm": 12, "mixed": 13}[kind])
+    N, per = _rows(w, depths, {"cold": 11, "warm": 12, "mixed": 13, "short1": 14, "short2": 15}[kind])
     log(f"case {kind}/{wdt}: depths {depths}, d={w.d} f={w.f}")
     ws = synth.all_expert_weights(w, 0, threads=4)
     ctx = make_context(w, max_tokens=N)
