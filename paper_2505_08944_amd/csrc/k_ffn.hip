@@ -16,14 +16,15 @@
 // dispatches workgroups round robin over the 8 XCDs, so workgroup w works on
 // slot (w % 8) * (grid / 8) + w / 8, giving each XCD (and its L2) a
 // contiguous run of tiles, and the big tiles of a group are ordered in panels
-// of 8 column tiles so that such a run is a compact block of row and column
-// tiles.
+// of 8 column tiles (4 in the down launch) so that such a run is a compact
+// block of row and column tiles.
 //
 // bf16 / fp8-weight path: 256-thread workgroups, K step 64, four waves each
 // owning a quadrant of the tile computed with v_mfma_f32_32x32x16_bf16 (f32
 // accumulate).  Tiles move from global memory straight into LDS (no staging
 // registers) through a ring of stages; the loads of later K steps are in
-// flight while the current one is multiplied.  Gate/up tiles hold BN/2
+// flight while the current one is multiplied, and the refill of a freed
+// stage is spread over the MFMAs that follow instead of issued as a block.  Gate/up tiles hold BN/2
 // features of W_gate and the same BN/2 of W_up, interleaved per wave quadrant,
 // so each lane finds the gate and up accumulator of the same (row, feature)
 // in its own registers and applies the SiLU-and-multiply epilogue without any
