@@ -368,9 +368,10 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   } while (0)
 
   // Two-stage rings (bf16 big tiles): the refill of the stage freed by a
-  // barrier (kNA + kNB loads per wave, listed A block 0, B block 0, A block
-  // 1, ...) goes out one load after every second MFMA of the 32 MFMAs that
-  // follow the barrier, i.e. over the first two operand groups of the step.
+  // barrier (kNA + kNB loads per wave, the kNB weight blocks first, which
+  // measured 2-4% faster than alternating A and B blocks) goes out one load
+  // after every second MFMA of the 32 MFMAs that follow the barrier, i.e.
+  // over the first two operand groups of the step.
   // Loads bunched after the barrier queue up at the address unit (four waves
   // issue theirs at once) and stall the issuing wave, and with it its matrix
   // pipe; spread this way they leave 32 MFMAs for the last load to land.
@@ -434,10 +435,10 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       __builtin_amdgcn_sched_barrier(0);                                                         \
       if (m_ % 2 == 1) {                                                                         \
         const int l_ = ((GB) + m_) / 2;                                                          \
-        if (l_ % 2 == 0)                                                                         \
-          dload16(rsA, aoff[l_ / 2], (LK) * kRowA, sa_ + (l_ / 2) * 1024);                       \
+        if (l_ < kNB)                                                                            \
+          dload16(rsB, boff[l_], (LK) * kRowB, sb_ + l_ * 1024);                                 \
         else                                                                                     \
-          dload16(rsB, boff[l_ / 2], (LK) * kRowB, sb_ + (l_ / 2) * 1024);                       \
+          dload16(rsA, aoff[l_ - kNB], (LK) * kRowA, sa_ + (l_ - kNB) * 1024);                   \
       }                                                                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \
