@@ -78,6 +78,11 @@ typedef struct {
                        /* workspace.  0: none.                                  */
 } aep_config;
 
+/* The library's context: one set of mu-queues (every layer), the expert
+ * weight tables and the batch in flight.  Opaque; created by aep_create,
+ * freed by aep_destroy, owned by the library. */
+typedef struct aep_ctx aep_ctx;
+
 /* A drained layer.  Filled by aep_rebatch; all pointers are device views into
  * the bound workspace and stay valid until aep_release_batch (or the next
  * aep_rebatch, which is refused while a batch is outstanding).
@@ -110,19 +115,19 @@ const char* aep_status_string(aep_status s);
  * AEP_ERR_UNSUPPORTED for a shape the kernels do not cover (d or f not a
  * multiple of 64; with BF16 activations, 2 * d * f bytes, or
  * 2 * max_tokens_per_layer * max(d, f) bytes, of 4 GiB or more). */
-aep_status aep_create(const aep_config* cfg, void** out);
+aep_status aep_create(const aep_config* cfg, aep_ctx** out);
 
 /* Destroy a context (NULL is allowed).  Does not free the caller's workspace. */
-aep_status aep_destroy(void* ctx);
+aep_status aep_destroy(aep_ctx* ctx);
 
 /* Bytes of device workspace this configuration needs (host only). */
-aep_status aep_workspace_size(const void* ctx, size_t* bytes);
+aep_status aep_workspace_size(const aep_ctx* ctx, size_t* bytes);
 
 /* Bind a caller-allocated device workspace of at least aep_workspace_size
  * bytes, 256-byte aligned, on the current HIP device.  Initialises it on
  * `stream` and waits for that.  Resets every queue.  The workspace holds the
  * mu-queues, weight tables, the batch buffers and the FFN intermediate. */
-aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream);
+aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stream);
 
 /* Register one expert's weights for a layer (pointers are borrowed and must
  * stay valid while the layer can run).  expert in [0, E) is routed; expert
@@ -132,7 +137,7 @@ aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream)
  *   channels) and scale_down [d_model], bf16: W = code * scale per output
  *   channel.  Scales must be NULL for other weight types.
  * Copies the pointer table to the device on `stream` and waits for it. */
-aep_status aep_set_expert_weights(void* ctx, int32_t layer, int32_t expert, const void* w_gate,
+aep_status aep_set_expert_weights(aep_ctx* ctx, int32_t layer, int32_t expert, const void* w_gate,
                                   const void* w_up, const void* w_down, const void* scale_gate_up,
                                   const void* scale_down, void* stream);
 
@@ -147,7 +152,7 @@ aep_status aep_set_expert_weights(void* ctx, int32_t layer, int32_t expert, cons
  * idx_out [T][k] int32 and w_out [T][k] f32 (device, may be NULL) receive
  * the routing.  T == 0 is a no-op.  AEP_ERR_CAPACITY if the layer could
  * exceed max_tokens_per_layer. */
-aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
+aep_status aep_route_enqueue(aep_ctx* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
                              int32_t* idx_out, float* w_out, void* stream);
 
 /* Receptor for rows routed elsewhere: appends n rows to queue (layer,
@@ -156,23 +161,28 @@ aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const floa
  * int32 in [0, k) (NULL: all 0), gate_w [n] f32.  The layer's token count
  * becomes max(current, n_tokens).  Not available on layers with shared
  * experts (AEP_ERR_UNSUPPORTED).  n == 0 is a no-op. */
-aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void* rows,
+aep_status aep_enqueue_rows(aep_ctx* ctx, int32_t layer, int32_t expert, const void* rows,
                             const int32_t* token_ids, const int32_t* slots, const float* gate_w,
                             int32_t n, int32_t n_tokens, void* stream);
 
 /* Host-side queue totals of a layer (no device access). */
-aep_status aep_queue_depth(const void* ctx, int32_t layer, int64_t* tokens, int64_t* rows);
+aep_status aep_queue_depth(const aep_ctx* ctx, int32_t layer, int64_t* tokens, int64_t* rows);
 
 /* Per-expert queue depths of a layer copied to host memory h_counts [E];
  * synchronises `stream`. */
-aep_status aep_expert_counts(void* ctx, int32_t layer, int32_t* h_counts, void* stream);
+aep_status aep_expert_counts(aep_ctx* ctx, int32_t layer, int32_t* h_counts, void* stream);
 
 /* Scheduler (Sec. 3.4): pick the next layer to drain from the host-side
- * queue totals.  MTFS: most queued rows (ties: lowest layer).  FLFS: lowest
- * non-empty layer.  DEFRAG: Algorithm 1 at layer granularity, score(b) =
- * rows(b) + sum_{i=1..lookahead} rows((b+i) mod n_layers) * delta^i, over
- * non-empty layers (ties: lowest).  AEP_ERR_EMPTY when nothing is queued. */
-aep_status aep_pick_layer(const void* ctx, int32_t policy, double delta, int32_t lookahead,
+ * queue totals rows(b) (no device access, no sync).  MTFS: most queued rows
+ * (ties: lowest layer).  FLFS: lowest non-empty layer.  DEFRAG: Algorithm 1
+ * at layer granularity -- a drain takes every expert of the layer and the
+ * host knows only layer totals, so each queue of Algorithm 1 is replaced by
+ * its layer's average rows(b) / n_experts and the score multiplied by
+ * n_experts: score(b) = rows(b) + sum_{i=1..lookahead} rows((b+i) mod
+ * n_layers) * delta^i over non-empty layers (ties: lowest).  delta >= 0 and
+ * finite, lookahead >= 0 (AEP_ERR_INVALID_ARG otherwise).  AEP_ERR_EMPTY
+ * (*layer untouched) when nothing is queued. */
+aep_status aep_pick_layer(const aep_ctx* ctx, int32_t policy, double delta, int32_t lookahead,
                           int32_t* layer);
 
 /* Scheduler over (block, expert) queues (Sec. 3.4, Algorithm 1), host only:
@@ -267,27 +277,27 @@ aep_status aep_sim_run(const aep_sim_config* cfg, aep_sim_trace* trace, aep_sim_
  * queued row into x_perm (a bit copy) -- and empty the layer's queues.  Fills
  * *out (host struct).  AEP_ERR_EMPTY if nothing is queued, AEP_ERR_STATE if
  * a batch is still outstanding or weights of the layer are missing. */
-aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream);
+aep_status aep_rebatch(aep_ctx* ctx, int32_t layer, aep_batch* out, void* stream);
 
 /* Expert FFN of a batch: every group g computes, on its rows,
  * y = W_down (silu(W_gate x) * (W_up x)), silu(v) = v / (1 + e^-v), with
  * f32 accumulation; the intermediate h is rounded to the act dtype.
  * y: device [n_rows][d] act dtype, caller-owned. */
-aep_status aep_expert_ffn(void* ctx, const aep_batch* batch, void* y, void* stream);
+aep_status aep_expert_ffn(aep_ctx* ctx, const aep_batch* batch, void* y, void* stream);
 
 /* The two halves of aep_expert_ffn, for callers that schedule (or time) them
  * separately.  aep_expert_gate_up computes h = silu(W_gate x) * (W_up x) for
  * every row of the batch into the workspace; aep_expert_down then computes
  * y = W_down h.  aep_expert_down must follow aep_expert_gate_up of the same
  * batch in stream order (the library does not check this). */
-aep_status aep_expert_gate_up(void* ctx, const aep_batch* batch, void* stream);
-aep_status aep_expert_down(void* ctx, const aep_batch* batch, void* y, void* stream);
+aep_status aep_expert_gate_up(aep_ctx* ctx, const aep_batch* batch, void* stream);
+aep_status aep_expert_down(aep_ctx* ctx, const aep_batch* batch, void* y, void* stream);
 
 /* Top-K merge (Sec. 3.2): out[t] = sum_{j<k} token_weight[t][j] *
  * y[token_pos[t][j]] (slots ascending, absent slots skipped) + sum_s
  * y[n_routed + s*n_tokens + t], accumulated in f32 and rounded once.
  * out: device [n_tokens][d] act dtype, caller-owned. */
-aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* out, void* stream);
+aep_status aep_combine(aep_ctx* ctx, const aep_batch* batch, const void* y, void* out, void* stream);
 
 /* ---- Token pool: top-K merge across drains (Sec. 3.2, top-K support) ----
  * With single-expert drains a token's k rows run in different drains; its
@@ -307,7 +317,7 @@ aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* o
  * claimed (not yet released), or out of range, sets the device error flag
  * (reported by aep_sync).  Capacity: every expert queue of the layer must have
  * room for T more rows (AEP_ERR_CAPACITY otherwise, nothing launched). */
-aep_status aep_route_enqueue_ids(void* ctx, int32_t layer, const void* x, const float* logits,
+aep_status aep_route_enqueue_ids(aep_ctx* ctx, int32_t layer, const void* x, const float* logits,
                                  int32_t T, const int32_t* token_ids, int32_t* idx_out, float* w_out,
                                  void* stream);
 
@@ -319,12 +329,12 @@ aep_status aep_route_enqueue_ids(void* ctx, int32_t layer, const void* x, const 
  * with aep_pool_accumulate (aep_combine refuses such a batch).
  * AEP_ERR_EMPTY when the expert's queue is known to be empty, AEP_ERR_STATE as
  * for aep_rebatch. */
-aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batch* out, void* stream);
+aep_status aep_rebatch_expert(aep_ctx* ctx, int32_t layer, int32_t expert, aep_batch* out, void* stream);
 
 /* pool[layer][row_token[r]] += row_weight[r] * y[r] (f32 fused multiply-add)
  * for every row r of a single-expert batch, and one more of that token's k
  * rows is merged.  y: device [n_rows][d] act dtype. */
-aep_status aep_pool_accumulate(void* ctx, const aep_batch* batch, const void* y, void* stream);
+aep_status aep_pool_accumulate(aep_ctx* ctx, const aep_batch* batch, const void* y, void* stream);
 
 /* Release every token of `layer` whose k rows have all been merged:
  * out[id] = the pool sum rounded once to the act dtype, the pool entry is
@@ -332,13 +342,13 @@ aep_status aep_pool_accumulate(void* ctx, const aep_batch* batch, const void* y,
  * token, 0 otherwise.  out: device [max_tokens_per_layer][d] act dtype (rows of
  * tokens not released are left untouched); ready: device int32
  * [max_tokens_per_layer] or NULL. */
-aep_status aep_pool_release(void* ctx, int32_t layer, void* out, int32_t* ready, void* stream);
+aep_status aep_pool_release(aep_ctx* ctx, int32_t layer, void* out, int32_t* ready, void* stream);
 
 /* Release a batch; its buffers may then be reused by the next aep_rebatch. */
-aep_status aep_release_batch(void* ctx, aep_batch* batch);
+aep_status aep_release_batch(aep_ctx* ctx, aep_batch* batch);
 
 /* Wait for `stream`, then report (and clear) the device error flag. */
-aep_status aep_sync(void* ctx, void* stream);
+aep_status aep_sync(aep_ctx* ctx, void* stream);
 
 /* Clock probe (instrumentation).  With d_buf a device array of 2 * n_pairs
  * uint64, every later bf16 / fp8-weight FFN launch of this context writes,
@@ -349,7 +359,7 @@ aep_status aep_sync(void* ctx, void* stream);
  * of a launch are at most the CU count.  d_buf = NULL (or n_pairs <= 0)
  * turns the probe off (the default).  The f32 path records nothing.  The
  * buffer is borrowed and must stay valid while the probe is on. */
-aep_status aep_set_clock_probe(void* ctx, uint64_t* d_buf, int32_t n_pairs);
+aep_status aep_set_clock_probe(aep_ctx* ctx, uint64_t* d_buf, int32_t n_pairs);
 
 /* Utility: decode n OCP e4m3fn codes (device) to bf16 (device); exact. */
 aep_status aep_fp8_e4m3_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stream);

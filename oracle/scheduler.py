@@ -3,21 +3,38 @@
 Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may use
 this module.
 
-* most-tokens-first-serve (MTFS, Sec. 3.4): run the queue holding the most
-  tokens.
-* first-layer-first-serve (FLFS, Sec. 3.4): run the lowest-numbered block that
-  holds any token.
-* defragging scheduler (Sec. 3.4, Algorithm 1): for block b the lookahead score
-  is sum_{i=1..L} (tokens queued in block (b+i) mod N_B / N_E) * delta^i; a
-  non-empty queue (b, e) scores lookahead(b) + Q[b][e]; the arg-max is run.
+Sec. 3.4 names two strawman policies and the defragging scheduler:
+
+* most-tokens-first-serve (MTFS): run the queue holding the most tokens;
+* first-layer-first-serve (FLFS): run the lowest-numbered block holding any
+  token;
+* defragging scheduler (Algorithm 1): every block b gets a lookahead term,
+  the queued load of the blocks after it (wrapping round to block 0), each
+  block's average queue per expert weighted by delta to the power of its
+  distance, over L blocks; a non-empty queue (b, e) scores its own depth plus
+  that term, and the best score runs.
+
+Written here as whole-table numpy expressions: the per-block average
+``Q.sum(1) / N_E``, the lookahead vector built from it by rolling it
+i = 1..L places and weighting it by delta^i, the score table ``Q + look``
+masked to non-empty queues, and the first maximum in row-major order.
 
 Readings where the algorithm is silent or inconsistent: the lookahead depth L
 is a parameter (the listing's bound clashes with the top-K symbol); the
-average uses N_E; ties go to the lowest (b, e) in row-major order; when every
-queue is empty there is nothing to run (None).  With delta = 0 the score is
-the queue depth alone, i.e. MTFS over (block, expert) queues.
+average divides by N_E; ties go to the lowest (b, e) in row-major order; when
+every queue is empty there is nothing to run (None).  With delta = 0 the score
+is the queue depth alone, i.e. MTFS over (block, expert) queues.  FLFS over
+(block, expert) queues runs the largest queue of the lowest non-empty block.
 
-Parity: pinned by tests/test_oracle_scheduler.py (hand-computed queue tables).
+Layer granularity (one GPU drains a whole block, every expert of it): the
+host knows each block's total R[b] without a device sync, so each queue of
+Algorithm 1 is replaced by its block's average R[b] / N_E and the score is
+multiplied by N_E: score(b) = R[b] + sum_{i=1..L} R[(b+i) mod N_B] delta^i.
+
+Parity: pinned by tests/test_oracle_scheduler.py (hand-worked score tables,
+delta = 0 equals MTFS, brute-force enumeration of tiny tables) and by the
+hand-traced runtime-model runs of tests/test_oracle_sim.py; planted mistakes
+in the decay, tie and FLFS-queue rules each fail one of those pins.
 """
 
 from __future__ import annotations
@@ -26,46 +43,92 @@ from typing import Optional, Sequence, Tuple
 
 import numpy as np
 
-__all__ = ["pick_mtfs", "pick_flfs", "defrag_scores", "pick_defrag"]
+__all__ = ["pick_mtfs", "pick_flfs", "lookahead_terms", "defrag_scores", "pick_defrag",
+           "pick_queue_mtfs", "pick_queue_flfs", "layer_scores", "pick_layer_defrag"]
+
+
+def _decay_weights(delta: float, lookahead: int) -> np.ndarray:
+    """delta^1 .. delta^L, each the previous times delta."""
+    return np.cumprod(np.full(int(lookahead), float(delta), dtype=np.float64))
+
+
+def _first_max(scores: np.ndarray) -> int:
+    """Index of the first largest entry (ties go to the lowest index)."""
+    return int(np.argmax(scores))
+
+
+def _largest_queue(row: np.ndarray) -> int:
+    """The largest queue of one block (ties: lowest expert id)."""
+    return _first_max(np.asarray(row))
 
 
 def pick_mtfs(rows: Sequence[int]) -> Optional[int]:
-    best, best_rows = None, 0
-    for b, r in enumerate(rows):
-        if r > best_rows:
-            best, best_rows = b, r
-    return best
+    """Index of the largest positive entry (ties: lowest), None if none."""
+    r = np.asarray(rows, dtype=np.int64)
+    if r.size == 0 or r.max() <= 0:
+        return None
+    return _first_max(r)
 
 
 def pick_flfs(rows: Sequence[int]) -> Optional[int]:
-    for b, r in enumerate(rows):
-        if r > 0:
-            return b
-    return None
+    """Lowest index holding any row, None if none."""
+    nz = np.flatnonzero(np.asarray(rows, dtype=np.int64) > 0)
+    return int(nz[0]) if nz.size else None
+
+
+def lookahead_terms(load: Sequence[float], delta: float, lookahead: int) -> np.ndarray:
+    """look[b] = sum_{i=1..L} load[(b + i) mod N_B] * delta^i (i ascending)."""
+    load = np.asarray(load, dtype=np.float64)
+    w = _decay_weights(delta, lookahead)
+    look = np.zeros_like(load)
+    for i in range(1, int(lookahead) + 1):
+        look = look + np.roll(load, -i) * w[i - 1]
+    return look
 
 
 def defrag_scores(Q: np.ndarray, delta: float, lookahead: int) -> np.ndarray:
+    """Algorithm 1's score of every (block, expert) queue; 0 for empty queues."""
     Q = np.asarray(Q, dtype=np.float64)
-    NB, NE = Q.shape
-    scores = np.zeros((NB, NE), dtype=np.float64)
-    for b in range(NB):
-        lscore = 0.0
-        for i in range(1, lookahead + 1):
-            lscore += (Q[(b + i) % NB].sum() / NE) * delta ** i
-        for e in range(NE):
-            if Q[b, e] > 0:
-                scores[b, e] = lscore + Q[b, e]
-    return scores
+    look = lookahead_terms(Q.sum(axis=1) / Q.shape[1], delta, lookahead)
+    return np.where(Q > 0, Q + look[:, None], 0.0)
 
 
 def pick_defrag(Q: np.ndarray, delta: float, lookahead: int) -> Optional[Tuple[int, int]]:
     Q = np.asarray(Q)
     if not np.any(Q > 0):
         return None
-    s = defrag_scores(Q, delta, lookahead)
-    best = None
-    for b in range(s.shape[0]):
-        for e in range(s.shape[1]):
-            if Q[b, e] > 0 and (best is None or s[b, e] > s[best]):
-                best = (b, e)
-    return best
+    s = np.where(Q > 0, defrag_scores(Q, delta, lookahead), -np.inf)
+    b, e = divmod(_first_max(s.ravel()), Q.shape[1])
+    return int(b), int(e)
+
+
+def pick_queue_mtfs(Q: np.ndarray) -> Optional[Tuple[int, int]]:
+    """MTFS over (block, expert) queues: the largest queue (row-major ties)."""
+    Q = np.asarray(Q, dtype=np.int64)
+    if not np.any(Q > 0):
+        return None
+    b, e = divmod(_first_max(Q.ravel()), Q.shape[1])
+    return int(b), int(e)
+
+
+def pick_queue_flfs(Q: np.ndarray) -> Optional[Tuple[int, int]]:
+    """FLFS over (block, expert) queues: the lowest block holding any row, and
+    its largest queue."""
+    Q = np.asarray(Q, dtype=np.int64)
+    b = pick_flfs(Q.sum(axis=1))
+    if b is None:
+        return None
+    return b, _largest_queue(Q[b])
+
+
+def layer_scores(rows: Sequence[int], delta: float, lookahead: int) -> np.ndarray:
+    """Layer-granularity defrag score of every block (0 for empty blocks)."""
+    R = np.asarray(rows, dtype=np.float64)
+    return np.where(R > 0, R + lookahead_terms(R, delta, lookahead), 0.0)
+
+
+def pick_layer_defrag(rows: Sequence[int], delta: float, lookahead: int) -> Optional[int]:
+    R = np.asarray(rows, dtype=np.int64)
+    if not np.any(R > 0):
+        return None
+    return _first_max(np.where(R > 0, layer_scores(R, delta, lookahead), -np.inf))

@@ -12,7 +12,9 @@ arriving over time), written with Python lists, dicts and heapq:
   routing stream gives u = draw mod (last CDF entry), and the expert is the
   first e with cdf[e] > u; repeated experts are skipped;
 * when the runtime is free and rows are queued (and the time is before the
-  horizon) the policy picks a (block, expert) queue or a whole block, whose
+  horizon) the policy picks a (block, expert) queue (oracle/scheduler.py:
+  pick_queue_mtfs, pick_queue_flfs, pick_defrag) or a whole block
+  (pick_mtfs, pick_flfs, pick_layer_defrag over block totals), whose
   rows are drained in queue order (experts in id order for a block); the step
   lasts (non-empty experts) * cost_fixed_us + ceil(rows * cost_row_ns / 1000);
 * at the end of the step every token whose last queued row of that block ran
@@ -26,8 +28,10 @@ arriving over time), written with Python lists, dicts and heapq:
 The generator is SplitMix64's output function (Steele, Lea, Flood 2014) on
 seed + stream * 0xD1B54A32D192ED03 + counter * 0x9E3779B97F4A7C15 mod 2^64.
 
-Parity: pinned by tests/test_oracle_sim.py (hand-traced runs, conservation
-laws, the SplitMix64 reference sequence) and compared step by step with the
+Parity: pinned by tests/test_oracle_sim.py (hand-traced runs at expert and
+block granularity under every policy, with the scores at the decisions where
+the policies part ways; conservation laws; the SplitMix64 reference
+sequence) and compared step by step with the
 library in tests/test_sched_host.py.
 """
 
@@ -36,7 +40,8 @@ from __future__ import annotations
 import heapq
 from typing import Dict, List, Sequence
 
-from .scheduler import pick_defrag, pick_flfs, pick_mtfs
+from .scheduler import (pick_defrag, pick_flfs, pick_layer_defrag, pick_mtfs, pick_queue_flfs,
+                        pick_queue_mtfs)
 
 MASK = (1 << 64) - 1
 GOLDEN = 0x9E3779B97F4A7C15
@@ -56,20 +61,10 @@ def draw(seed: int, stream: int, counter: int) -> int:
 
 
 def _pick_queue(Q: List[List[int]], policy: str, delta: float, lookahead: int):
-    NB, NE = len(Q), len(Q[0])
     if policy == "mtfs":
-        best = None
-        for b in range(NB):
-            for e in range(NE):
-                if Q[b][e] > 0 and (best is None or Q[b][e] > Q[best[0]][best[1]]):
-                    best = (b, e)
-        return best
+        return pick_queue_mtfs(Q)
     if policy == "flfs":
-        b = pick_flfs([sum(row) for row in Q])
-        if b is None:
-            return None
-        e = max(range(NE), key=lambda x: (Q[b][x], -x))
-        return (b, e)
+        return pick_queue_flfs(Q)
     return pick_defrag(Q, delta, lookahead)
 
 
@@ -78,20 +73,7 @@ def _pick_block(R: List[int], policy: str, delta: float, lookahead: int):
         return pick_mtfs(R)
     if policy == "flfs":
         return pick_flfs(R)
-    NB = len(R)
-    best, best_score = None, 0.0
-    for b in range(NB):
-        if R[b] <= 0:
-            continue
-        score, weight = float(R[b]), 1.0
-        look = 0.0
-        for i in range(1, lookahead + 1):
-            weight *= delta
-            look += float(R[(b + i) % NB]) * weight
-        score = look + float(R[b])
-        if best is None or score > best_score:
-            best, best_score = b, score
-    return best
+    return pick_layer_defrag(R, delta, lookahead)
 
 
 def simulate(*, n_blocks: int, n_experts: int, top_k: int, n_frag: int, granularity: str, policy: str,

@@ -85,6 +85,12 @@ constexpr int kTallBM = 256;            // family 1 of a cold batch: 256 rows x 
 constexpr int kBM32 = 64;
 constexpr int kBN32 = 64;
 
+// Layer-granularity pick (host): the block to drain next from per-block
+// totals R[nb] under an aep_policy (defrag: R[b] + sum_{i=1..lookahead}
+// R[(b + i) mod nb] * delta^i).  Ties go to the lowest block; false when every
+// block is empty.  Defined with the host scheduler (sched.hip).
+bool pick_block(const int64_t* R, int nb, int policy, double delta, int lookahead, int* pb);
+
 // ---------------------------------------------------------------- launchers
 // Each returns hipGetLastError() after the launch.
 hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,

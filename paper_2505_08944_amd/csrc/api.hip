@@ -34,7 +34,10 @@ struct LayerState {
   }
 };
 
-struct Ctx {
+}  // namespace
+
+// The opaque context of include/aep.h.
+struct aep_ctx {
   aep_config cfg{};
   int G = 0;
   int esz = 0;  // bytes per activation element
@@ -83,6 +86,10 @@ struct Ctx {
   }
 };
 
+namespace {
+
+using Ctx = aep_ctx;
+
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 bool layout(Ctx& c) {
@@ -126,8 +133,8 @@ bool layout(Ctx& c) {
   return true;
 }
 
-Ctx* as_ctx(void* p) { return reinterpret_cast<Ctx*>(p); }
-const Ctx* as_ctx(const void* p) { return reinterpret_cast<const Ctx*>(p); }
+Ctx* as_ctx(aep_ctx* p) { return p; }
+const Ctx* as_ctx(const aep_ctx* p) { return p; }
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE; }
@@ -174,7 +181,7 @@ const char* aep_status_string(aep_status s) {
   return "AEP_ERR_UNKNOWN";
 }
 
-aep_status aep_create(const aep_config* cfg, void** out) {
+aep_status aep_create(const aep_config* cfg, aep_ctx** out) {
   if (!cfg || !out) return AEP_ERR_INVALID_ARG;
   const aep_config& g = *cfg;
   if (g.n_layers < 1 || g.n_experts < 1 || g.n_shared < 0 ||
@@ -217,18 +224,18 @@ aep_status aep_create(const aep_config* cfg, void** out) {
   return AEP_OK;
 }
 
-aep_status aep_destroy(void* ctx) {
+aep_status aep_destroy(aep_ctx* ctx) {
   delete as_ctx(ctx);
   return AEP_OK;
 }
 
-aep_status aep_workspace_size(const void* ctx, size_t* bytes) {
+aep_status aep_workspace_size(const aep_ctx* ctx, size_t* bytes) {
   if (!ctx || !bytes) return AEP_ERR_INVALID_ARG;
   *bytes = as_ctx(ctx)->ws_need;
   return AEP_OK;
 }
 
-aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream) {
+aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || !d_ws) return AEP_ERR_INVALID_ARG;
   if (reinterpret_cast<uintptr_t>(d_ws) & 255) return AEP_ERR_INVALID_ARG;
@@ -261,7 +268,7 @@ aep_status aep_bind_workspace(void* ctx, void* d_ws, size_t bytes, void* stream)
   return AEP_OK;
 }
 
-aep_status aep_set_expert_weights(void* ctx, int32_t layer, int32_t expert, const void* w_gate,
+aep_status aep_set_expert_weights(aep_ctx* ctx, int32_t layer, int32_t expert, const void* w_gate,
                                   const void* w_up, const void* w_down, const void* scale_gate_up,
                                   const void* scale_down, void* stream) {
   Ctx* c = as_ctx(ctx);
@@ -326,12 +333,12 @@ static aep_status route_common(Ctx* c, int32_t layer, const void* x, const float
   return AEP_OK;
 }
 
-aep_status aep_route_enqueue(void* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
+aep_status aep_route_enqueue(aep_ctx* ctx, int32_t layer, const void* x, const float* logits, int32_t T,
                              int32_t* idx_out, float* w_out, void* stream) {
   return route_common(as_ctx(ctx), layer, x, logits, T, nullptr, idx_out, w_out, stream);
 }
 
-aep_status aep_route_enqueue_ids(void* ctx, int32_t layer, const void* x, const float* logits,
+aep_status aep_route_enqueue_ids(aep_ctx* ctx, int32_t layer, const void* x, const float* logits,
                                  int32_t T, const int32_t* token_ids, int32_t* idx_out, float* w_out,
                                  void* stream) {
   if (T > 0 && !token_ids) return AEP_ERR_INVALID_ARG;
@@ -340,7 +347,7 @@ aep_status aep_route_enqueue_ids(void* ctx, int32_t layer, const void* x, const 
   return route_common(c, layer, x, logits, T, T > 0 ? token_ids : nullptr, idx_out, w_out, stream);
 }
 
-aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void* rows,
+aep_status aep_enqueue_rows(aep_ctx* ctx, int32_t layer, int32_t expert, const void* rows,
                             const int32_t* token_ids, const int32_t* slots, const float* gate_w,
                             int32_t n, int32_t n_tokens, void* stream) {
   Ctx* c = as_ctx(ctx);
@@ -370,7 +377,7 @@ aep_status aep_enqueue_rows(void* ctx, int32_t layer, int32_t expert, const void
   return AEP_OK;
 }
 
-aep_status aep_queue_depth(const void* ctx, int32_t layer, int64_t* tokens, int64_t* rows) {
+aep_status aep_queue_depth(const aep_ctx* ctx, int32_t layer, int64_t* tokens, int64_t* rows) {
   const Ctx* c = as_ctx(ctx);
   if (!c || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
   if (tokens) *tokens = c->layers[layer].tokens;
@@ -378,7 +385,7 @@ aep_status aep_queue_depth(const void* ctx, int32_t layer, int64_t* tokens, int6
   return AEP_OK;
 }
 
-aep_status aep_expert_counts(void* ctx, int32_t layer, int32_t* h_counts, void* stream) {
+aep_status aep_expert_counts(aep_ctx* ctx, int32_t layer, int32_t* h_counts, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || !h_counts || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
   if (!c->ws) return AEP_ERR_STATE;
@@ -389,55 +396,22 @@ aep_status aep_expert_counts(void* ctx, int32_t layer, int32_t* h_counts, void* 
   return dev(hipStreamSynchronize(s));
 }
 
-aep_status aep_pick_layer(const void* ctx, int32_t policy, double delta, int32_t lookahead,
+aep_status aep_pick_layer(const aep_ctx* ctx, int32_t policy, double delta, int32_t lookahead,
                           int32_t* layer) {
   const Ctx* c = as_ctx(ctx);
   if (!c || !layer) return AEP_ERR_INVALID_ARG;
-  const int NB = c->cfg.n_layers;
-  bool any = false;
-  for (const auto& l : c->layers) any = any || l.rows > 0;
-  if (policy == AEP_POLICY_MTFS) {
-    if (!any) return AEP_ERR_EMPTY;
-    int best = -1;
-    for (int b = 0; b < NB; ++b)
-      if (c->layers[b].rows > 0 && (best < 0 || c->layers[b].rows > c->layers[best].rows)) best = b;
-    *layer = best;
-    return AEP_OK;
-  }
-  if (policy == AEP_POLICY_FLFS) {
-    if (!any) return AEP_ERR_EMPTY;
-    for (int b = 0; b < NB; ++b)
-      if (c->layers[b].rows > 0) {
-        *layer = b;
-        return AEP_OK;
-      }
-    return AEP_ERR_EMPTY;
-  }
-  if (policy == AEP_POLICY_DEFRAG) {
-    if (lookahead < 0 || !(delta >= 0.0) || !std::isfinite(delta)) return AEP_ERR_INVALID_ARG;
-    if (!any) return AEP_ERR_EMPTY;
-    int best = -1;
-    double best_s = 0.0;
-    for (int b = 0; b < NB; ++b) {
-      if (c->layers[b].rows <= 0) continue;
-      double ls = 0.0, pw = 1.0;
-      for (int i = 1; i <= lookahead; ++i) {
-        pw *= delta;
-        ls += (double)c->layers[(b + i) % NB].rows * pw;
-      }
-      const double sc = ls + (double)c->layers[b].rows;
-      if (best < 0 || sc > best_s) {
-        best = b;
-        best_s = sc;
-      }
-    }
-    *layer = best;
-    return AEP_OK;
-  }
-  return AEP_ERR_INVALID_ARG;
+  if (policy < AEP_POLICY_MTFS || policy > AEP_POLICY_DEFRAG) return AEP_ERR_INVALID_ARG;
+  if (policy == AEP_POLICY_DEFRAG && (lookahead < 0 || !(delta >= 0.0) || !std::isfinite(delta)))
+    return AEP_ERR_INVALID_ARG;
+  std::vector<int64_t> rows(c->layers.size());
+  for (size_t b = 0; b < rows.size(); ++b) rows[b] = c->layers[b].rows;
+  int pb = -1;
+  if (!pick_block(rows.data(), (int)rows.size(), policy, delta, lookahead, &pb)) return AEP_ERR_EMPTY;
+  *layer = pb;
+  return AEP_OK;
 }
 
-aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
+aep_status aep_rebatch(aep_ctx* ctx, int32_t layer, aep_batch* out, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || !out || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
   if (!c->ws || c->batch_out) return AEP_ERR_STATE;
@@ -483,7 +457,7 @@ aep_status aep_rebatch(void* ctx, int32_t layer, aep_batch* out, void* stream) {
   return AEP_OK;
 }
 
-aep_status aep_rebatch_expert(void* ctx, int32_t layer, int32_t expert, aep_batch* out, void* stream) {
+aep_status aep_rebatch_expert(aep_ctx* ctx, int32_t layer, int32_t expert, aep_batch* out, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || !out || layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->cfg.n_experts)
     return AEP_ERR_INVALID_ARG;
@@ -560,7 +534,7 @@ static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, 
                         c->clk, c->clk_n, as_stream(stream)));
 }
 
-aep_status aep_set_clock_probe(void* ctx, uint64_t* d_buf, int32_t n_pairs) {
+aep_status aep_set_clock_probe(aep_ctx* ctx, uint64_t* d_buf, int32_t n_pairs) {
   Ctx* c = as_ctx(ctx);
   if (!c) return AEP_ERR_INVALID_ARG;
   const bool on = d_buf != nullptr && n_pairs > 0;
@@ -569,22 +543,22 @@ aep_status aep_set_clock_probe(void* ctx, uint64_t* d_buf, int32_t n_pairs) {
   return AEP_OK;
 }
 
-aep_status aep_expert_gate_up(void* ctx, const aep_batch* batch, void* stream) {
+aep_status aep_expert_gate_up(aep_ctx* ctx, const aep_batch* batch, void* stream) {
   return ffn_stage(as_ctx(ctx), batch, 0, nullptr, stream);
 }
 
-aep_status aep_expert_down(void* ctx, const aep_batch* batch, void* y, void* stream) {
+aep_status aep_expert_down(aep_ctx* ctx, const aep_batch* batch, void* y, void* stream) {
   return ffn_stage(as_ctx(ctx), batch, 1, y, stream);
 }
 
-aep_status aep_expert_ffn(void* ctx, const aep_batch* batch, void* y, void* stream) {
+aep_status aep_expert_ffn(aep_ctx* ctx, const aep_batch* batch, void* y, void* stream) {
   if (!y) return check_batch(as_ctx(ctx), batch) == AEP_OK ? AEP_ERR_INVALID_ARG : check_batch(as_ctx(ctx), batch);
   aep_status st = ffn_stage(as_ctx(ctx), batch, 0, nullptr, stream);
   if (st != AEP_OK) return st;
   return ffn_stage(as_ctx(ctx), batch, 1, y, stream);
 }
 
-aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* out, void* stream) {
+aep_status aep_combine(aep_ctx* ctx, const aep_batch* batch, const void* y, void* out, void* stream) {
   Ctx* c = as_ctx(ctx);
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
@@ -595,7 +569,7 @@ aep_status aep_combine(void* ctx, const aep_batch* batch, const void* y, void* o
                             as_stream(stream)));
 }
 
-aep_status aep_pool_accumulate(void* ctx, const aep_batch* batch, const void* y, void* stream) {
+aep_status aep_pool_accumulate(aep_ctx* ctx, const aep_batch* batch, const void* y, void* stream) {
   Ctx* c = as_ctx(ctx);
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
@@ -606,7 +580,7 @@ aep_status aep_pool_accumulate(void* ctx, const aep_batch* batch, const void* y,
                                     c->pend(batch->layer), c->cfg.d_model, as_stream(stream)));
 }
 
-aep_status aep_pool_release(void* ctx, int32_t layer, void* out, int32_t* ready, void* stream) {
+aep_status aep_pool_release(aep_ctx* ctx, int32_t layer, void* out, int32_t* ready, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
   if (!c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
@@ -616,7 +590,7 @@ aep_status aep_pool_release(void* ctx, int32_t layer, void* out, int32_t* ready,
                                  (int)c->tmax(), out, ready, c->cfg.d_model, as_stream(stream)));
 }
 
-aep_status aep_release_batch(void* ctx, aep_batch* batch) {
+aep_status aep_release_batch(aep_ctx* ctx, aep_batch* batch) {
   Ctx* c = as_ctx(ctx);
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
@@ -627,7 +601,7 @@ aep_status aep_release_batch(void* ctx, aep_batch* batch) {
   return AEP_OK;
 }
 
-aep_status aep_sync(void* ctx, void* stream) {
+aep_status aep_sync(aep_ctx* ctx, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c) return AEP_ERR_INVALID_ARG;
   if (!c->ws) return AEP_ERR_STATE;

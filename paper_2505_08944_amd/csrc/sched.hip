@@ -31,6 +31,7 @@
 #include <vector>
 
 #include "aep.h"
+#include "aep_internal.h"
 
 namespace {
 
@@ -46,49 +47,80 @@ uint64_t draw(uint64_t seed, uint64_t stream, uint64_t counter) {
   return mix64(seed + stream * 0xD1B54A32D192ED03ull + counter * 0x9E3779B97F4A7C15ull);
 }
 
-// Policy pick over a row-major table Q[nb][ne] of queued rows.  Returns false
-// when every queue is empty.
+// Weights of the lookahead blocks: delta^1 .. delta^L, each the previous
+// times delta.
+std::vector<double> decay_weights(double delta, int lookahead) {
+  std::vector<double> w((size_t)std::max(lookahead, 0));
+  double pw = 1.0;
+  for (auto& x : w) x = (pw *= delta);
+  return w;
+}
+
+// Lookahead term of every block: the loads of the blocks after it (wrapping
+// round), weighted by the decay of their distance, distances in ascending
+// order.
+std::vector<double> lookahead_terms(const std::vector<double>& load, double delta, int lookahead) {
+  const int nb = (int)load.size();
+  const std::vector<double> w = decay_weights(delta, lookahead);
+  std::vector<double> look((size_t)nb, 0.0);
+  for (int b = 0; b < nb; ++b)
+    for (int i = 1; i <= lookahead; ++i) look[b] += load[(b + i) % nb] * w[i - 1];
+  return look;
+}
+
+// Policy pick over a row-major table Q[nb][ne] of queued rows, evaluated one
+// block at a time.  Every policy only ever runs the largest queue of some
+// block (lowest expert on ties): MTFS compares those largest queues, FLFS takes
+// the lowest non-empty block, and Algorithm 1 adds each block's lookahead term
+// -- the average queue per expert of the blocks after it -- to its largest
+// queue.  Blocks are compared with a strict "greater", so ties go to the lowest
+// (block, expert).  Returns false when every queue is empty.
 bool pick_queue(const int64_t* Q, int nb, int ne, int policy, double delta, int lookahead, int* pb,
                 int* pe) {
-  int bb = -1, be = -1;
-  if (policy == AEP_POLICY_MTFS) {
-    for (int b = 0; b < nb; ++b)
-      for (int e = 0; e < ne; ++e)
-        if (Q[b * ne + e] > 0 && (bb < 0 || Q[b * ne + e] > Q[bb * ne + be])) bb = b, be = e;
-  } else if (policy == AEP_POLICY_FLFS) {
-    for (int b = 0; b < nb && bb < 0; ++b)
-      for (int e = 0; e < ne; ++e)
-        if (Q[b * ne + e] > 0 && (bb < 0 || Q[b * ne + e] > Q[bb * ne + be])) bb = b, be = e;
-  } else {
-    double best = 0.0;
-    for (int b = 0; b < nb; ++b) {
-      // lookahead score: average queued rows per expert of the next blocks,
-      // decayed by delta per block of distance
-      double ls = 0.0, pw = 1.0;
-      for (int i = 1; i <= lookahead; ++i) {
-        pw *= delta;
-        const int b2 = (b + i) % nb;
-        int64_t total = 0;
-        for (int e = 0; e < ne; ++e) total += Q[b2 * ne + e];
-        ls += ((double)total / (double)ne) * pw;
-      }
-      for (int e = 0; e < ne; ++e) {
-        if (Q[b * ne + e] <= 0) continue;
-        const double sc = ls + (double)Q[b * ne + e];
-        if (bb < 0 || sc > best) bb = b, be = e, best = sc;
-      }
+  std::vector<int64_t> total((size_t)nb, 0), top_q((size_t)nb, 0);
+  std::vector<int> top_e((size_t)nb, 0);
+  for (int b = 0; b < nb; ++b) {
+    const int64_t* row = Q + (size_t)b * ne;
+    for (int e = 0; e < ne; ++e) {
+      total[b] += row[e];
+      if (row[e] > top_q[b]) top_q[b] = row[e], top_e[b] = e;
     }
+  }
+  std::vector<double> bonus((size_t)nb, 0.0);
+  if (policy == AEP_POLICY_DEFRAG) {
+    std::vector<double> avg((size_t)nb);
+    for (int b = 0; b < nb; ++b) avg[b] = (double)total[b] / (double)ne;
+    bonus = lookahead_terms(avg, delta, lookahead);
+  }
+  int bb = -1;
+  double best = 0.0;
+  for (int b = 0; b < nb; ++b) {
+    if (top_q[b] <= 0) continue;
+    if (policy == AEP_POLICY_FLFS) {
+      bb = b;
+      break;
+    }
+    const double sc = (double)top_q[b] + bonus[b];
+    if (bb < 0 || sc > best) bb = b, best = sc;
   }
   if (bb < 0) return false;
   *pb = bb;
-  *pe = be;
+  *pe = top_e[bb];
   return true;
 }
 
-// Block-granularity pick over per-block totals R[nb] (the layer-level form of
-// the same policies; the defragging score scales Algorithm 1 by n_experts:
-// own rows + sum_i rows(b + i) * delta^i).
+}  // namespace
+
+namespace aep {
+
+// Block-granularity pick over per-block totals R[nb] (a whole block drains,
+// every expert of it).  The host knows only block totals without a device
+// sync, so Algorithm 1's queue depth is replaced by the block's average queue
+// R[b] / N_E and the score scaled by N_E: R[b] + sum_i R[(b + i) mod nb] *
+// delta^i.
 bool pick_block(const int64_t* R, int nb, int policy, double delta, int lookahead, int* pb) {
+  std::vector<double> bonus((size_t)nb, 0.0);
+  if (policy == AEP_POLICY_DEFRAG) bonus = lookahead_terms(std::vector<double>(R, R + nb), delta, lookahead);
   int bb = -1;
   double best = 0.0;
   for (int b = 0; b < nb; ++b) {
@@ -97,21 +129,17 @@ bool pick_block(const int64_t* R, int nb, int policy, double delta, int lookahea
       bb = b;
       break;
     }
-    double sc = (double)R[b];
-    if (policy == AEP_POLICY_DEFRAG) {
-      double ls = 0.0, pw = 1.0;
-      for (int i = 1; i <= lookahead; ++i) {
-        pw *= delta;
-        ls += (double)R[(b + i) % nb] * pw;
-      }
-      sc = ls + (double)R[b];
-    }
+    const double sc = bonus[b] + (double)R[b];
     if (bb < 0 || sc > best) bb = b, best = sc;
   }
   if (bb < 0) return false;
   *pb = bb;
   return true;
 }
+
+}  // namespace aep
+
+namespace {
 
 bool bad_policy(int32_t policy, double delta, int32_t lookahead) {
   if (policy < AEP_POLICY_MTFS || policy > AEP_POLICY_DEFRAG) return true;
@@ -240,7 +268,7 @@ aep_status aep_sim_run(const aep_sim_config* cfg, aep_sim_trace* trace, aep_sim_
       if (c.granularity == 0)
         pick_queue(tab.data(), NB, NE, c.policy, c.delta, c.lookahead, &pb, &pe);
       else
-        pick_block(R.data(), NB, c.policy, c.delta, c.lookahead, &pb);
+        aep::pick_block(R.data(), NB, c.policy, c.delta, c.lookahead, &pb);
       // drain
       drained.clear();
       int nonempty = 0;

@@ -14,6 +14,7 @@ import os
 import numpy as np
 import pytest
 
+from oracle import scheduler as osched
 from oracle import sim
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -101,3 +102,43 @@ def test_conservation_laws(seed, granularity, policy):
         assert r["done_us"][i] - arr[i] >= (ol[i] * NB - 1) * 150
     t = r["trace"]["t_start"]
     assert all(b >= a for a, b in zip(t, t[1:]))
+
+
+TRACES = json.load(open(os.path.join(GOLDEN, "sim_hand_traces.json")))
+
+
+def _run_traced(spec, base=TRACES["base"]):
+    kw = {k: v for k, v in base.items()}
+    return sim.simulate(**kw, granularity=spec["granularity"], policy=spec["policy"], delta=spec["delta"],
+                        lookahead=spec["lookahead"], arrival_us=spec["arrival_us"], out_len=spec["out_len"])
+
+
+@pytest.mark.parametrize("spec", TRACES["runs"], ids=[r["name"] for r in TRACES["runs"]])
+def test_hand_traced_policy_runs(spec):
+    """Block and expert granularity, three blocks, two experts: every step of
+    the hand trace (time, block, expert, rows, queue state), completion times,
+    and the scores at the decisions where the policies part ways."""
+    r = _run_traced(spec)
+    tr = r["trace"]
+    assert tr["t_start"] == spec["t_start"]
+    assert tr["block"] == spec["block"]
+    assert tr["rows"] == spec["rows"]
+    if "expert" in spec:
+        assert tr["expert"] == spec["expert"]
+    else:
+        assert set(tr["expert"]) == {-1}
+    if "block_rows_after" in spec:
+        assert tr["block_rows_after"] == spec["block_rows_after"]
+    assert r["done_us"] == spec["done_us"]
+    for dcs in spec["decisions"]:
+        i = spec["t_start"].index(dcs["t"])
+        if "R" in dcs:
+            assert spec["block"][i] == dcs["pick"]
+            if "scores" in dcs:
+                np.testing.assert_allclose(osched.layer_scores(dcs["R"], spec["delta"], spec["lookahead"]),
+                                           dcs["scores"], rtol=0, atol=1e-12)
+        else:
+            assert [spec["block"][i], spec["expert"][i]] == dcs["pick"]
+            if "scores" in dcs:
+                np.testing.assert_allclose(osched.defrag_scores(np.array(dcs["Q"]), spec["delta"], spec["lookahead"]),
+                                           dcs["scores"], rtol=0, atol=1e-12)

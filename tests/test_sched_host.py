@@ -16,15 +16,9 @@ from paper_2505_08944_amd import AEPError, sched
 
 def _oracle_pick(Q, policy, delta, lookahead):
     if policy == "mtfs":
-        best = None
-        for b in range(Q.shape[0]):
-            for e in range(Q.shape[1]):
-                if Q[b, e] > 0 and (best is None or Q[b, e] > Q[best]):
-                    best = (b, e)
-        return best
+        return osched.pick_queue_mtfs(Q)
     if policy == "flfs":
-        b = osched.pick_flfs(Q.sum(axis=1).tolist())
-        return None if b is None else (b, int(np.argmax(Q[b])))
+        return osched.pick_queue_flfs(Q)
     return osched.pick_defrag(Q, delta, lookahead)
 
 
@@ -34,7 +28,7 @@ def test_sched_pick_matches_oracle(policy):
     for trial in range(300):
         nb, ne = int(rng.integers(1, 9)), int(rng.integers(1, 9))
         Q = rng.integers(0, 6, (nb, ne)) * (rng.random((nb, ne)) < 0.5)
-        delta = [0.0, 0.25, 0.5, 0.75][trial % 4]
+        delta = [0.0, 0.25, 0.5, 0.75, 0.9, 1.0][trial % 6]
         la = int(rng.integers(0, 4))
         assert sched.sched_pick(Q, policy, delta, la) == _oracle_pick(Q, policy, delta, la), (Q, delta, la)
 
@@ -96,3 +90,25 @@ def test_sim_trace_capacity_and_invalid():
             sched.sim_run(**{**kw, **bad}, arrival_us=arr, out_len=ol, expert_cdf=cdf)
     with pytest.raises(AEPError):   # arrivals out of order
         sched.sim_run(**kw, arrival_us=arr[::-1].copy(), out_len=ol, expert_cdf=cdf)
+
+
+def test_sim_reproduces_hand_traces():
+    """The library's model runs the hand-traced runs of tests/golden/ step for
+    step (three blocks, two experts; FLFS, MTFS and the defragging scheduler
+    at block and expert granularity)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "sim_hand_traces.json")))
+    base = g["base"]
+    for spec in g["runs"]:
+        got = sched.sim_run(**{k: v for k, v in base.items() if k != "expert_cdf"}, granularity=spec["granularity"],
+                            policy=spec["policy"], delta=spec["delta"], lookahead=spec["lookahead"],
+                            arrival_us=np.array(spec["arrival_us"]), out_len=np.array(spec["out_len"]),
+                            expert_cdf=np.array(base["expert_cdf"]), trace_capacity=1000)
+        tr = got["trace"]
+        assert tr["t_start"].tolist() == spec["t_start"], spec["name"]
+        assert tr["block"].tolist() == spec["block"], spec["name"]
+        assert tr["rows"].tolist() == spec["rows"], spec["name"]
+        if "expert" in spec:
+            assert tr["expert"].tolist() == spec["expert"], spec["name"]
+        assert got["done_us"].tolist() == spec["done_us"], spec["name"]
