@@ -103,6 +103,7 @@ class Context:
         nbytes = ctypes.c_size_t()
         L.check(self.lib.aep_workspace_size(self.h, ctypes.byref(nbytes)), "aep_workspace_size")
         dev = device or torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
         # 256-byte alignment: over-allocate and slice
         raw = torch.empty(nbytes.value + 256, dtype=torch.uint8, device=dev)
         pad = (-raw.data_ptr()) % 256
@@ -110,6 +111,7 @@ class Context:
         self.workspace = raw[pad:pad + nbytes.value]
         L.check(self.lib.aep_bind_workspace(self.h, self.workspace.data_ptr(), nbytes.value, _stream()),
                 "aep_bind_workspace")
+        self.workspace_need = nbytes.value
         self._frag_refs: Dict[int, List[torch.Tensor]] = {l: [] for l in range(n_layers)}
         self._w_refs: Dict[Tuple[int, int], Tuple[torch.Tensor, ...]] = {}
 
@@ -121,7 +123,7 @@ class Context:
 
     @property
     def workspace_bytes(self) -> int:
-        return self.workspace.numel()
+        return self.workspace_need
 
     # ------------------------------------------------------------- weights
     def set_expert_weights(self, layer: int, expert: int, gate: torch.Tensor, up: torch.Tensor,
@@ -243,7 +245,7 @@ class Context:
 
     def expert_ffn(self, batch: BatchView, y: Optional[torch.Tensor] = None) -> torch.Tensor:
         if y is None:
-            y = torch.empty((batch.n_rows, self.d_model), dtype=self.act_torch, device=self.workspace.device)
+            y = torch.empty((batch.n_rows, self.d_model), dtype=self.act_torch, device=self.device)
         _need(y, "y", self.act_torch, (batch.n_rows, self.d_model))
         L.check(self.lib.aep_expert_ffn(self.h, ctypes.byref(batch.c), y.data_ptr(), _stream()), "aep_expert_ffn")
         return y
@@ -253,7 +255,7 @@ class Context:
 
     def expert_down(self, batch: BatchView, y: Optional[torch.Tensor] = None) -> torch.Tensor:
         if y is None:
-            y = torch.empty((batch.n_rows, self.d_model), dtype=self.act_torch, device=self.workspace.device)
+            y = torch.empty((batch.n_rows, self.d_model), dtype=self.act_torch, device=self.device)
         _need(y, "y", self.act_torch, (batch.n_rows, self.d_model))
         L.check(self.lib.aep_expert_down(self.h, ctypes.byref(batch.c), y.data_ptr(), _stream()), "aep_expert_down")
         return y

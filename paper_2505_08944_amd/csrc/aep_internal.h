@@ -93,17 +93,21 @@ bool pick_block(const int64_t* R, int nb, int policy, double delta, int lookahea
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipGetLastError() after the launch.
+// Routes T tokens; blockcnt [ceil(T / kRouteTokens)][E] receives the first
+// queue slot of each router workgroup's rows per expert and depth_nxt the new
+// depths (depth_cur + this fragment's counts).  done: a launch counter that
+// must be 0 before the launch (the kernel leaves it 0).
 hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,
                         float* r_w, int32_t* r_rank, int32_t* blockcnt, int32_t* idx_out,
-                        float* w_out, int32_t* err, hipStream_t s);
+                        float* w_out, const int32_t* depth_cur, int32_t* depth_nxt, int32_t* done,
+                        int32_t* err, hipStream_t s);
 // token_ids == nullptr: token t of the fragment is token_base + t.  Else its
 // id is token_ids[t] (< n_ids) and it claims pool entry live[id] / pend[id].
 hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* r_rank,
-                         const int32_t* blockcnt, int T, int E, int k, const char* x,
-                         int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
-                         int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
-                         const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
-                         int32_t* err, hipStream_t s);
+                         const int32_t* first_slot, int T, int E, int k, const char* x,
+                         int64_t row_bytes, int32_t token_base, QEntry* q, int64_t q_stride,
+                         const void** tok_row, const int32_t* token_ids, int n_ids, int32_t* live,
+                         int32_t* pend, int32_t* err, hipStream_t s);
 hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_t* token_ids,
                                const int32_t* slots, const float* gate_w, int n, int n_tokens,
                                int k, int expert, int E, const int32_t* depth_cur,

@@ -63,6 +63,8 @@ struct aep_ctx {
   int64_t tmax() const { return cfg.max_tokens_per_layer; }
   int64_t row_cap() const { return tmax() * cfg.top_k; }
   int32_t* err() const { return reinterpret_cast<int32_t*>(ws + off_err); }
+  // router launch counter (last-workgroup scan), in the error-flag block
+  int32_t* route_done() const { return reinterpret_cast<int32_t*>(ws + off_err) + 16; }
   int32_t* depth(int layer, int half) const {
     return reinterpret_cast<int32_t*>(ws + off_depth) + ((int64_t)layer * 2 + half) * cfg.n_experts;
   }
@@ -138,6 +140,36 @@ const Ctx* as_ctx(const aep_ctx* p) { return p; }
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE; }
+
+// A workspace is bound.
+bool ws_bound(const Ctx* c) { return c->ws != nullptr; }
+
+// Initialise the caller's workspace ws on stream s and
+// reset every queue of c.
+aep_status bind(Ctx* c, char* ws, int devid, hipStream_t s) {
+  int ncu = 0;
+  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, devid) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  // clear the error flag and launch counter, every depth counter and the weight tables
+  if (hipMemsetAsync(ws + c->off_err, 0, c->off_q - c->off_err, s) != hipSuccess) return AEP_ERR_DEVICE;
+  if (hipMemsetAsync(ws + c->off_wtab, 0, sizeof(WeightDesc) * c->cfg.n_layers * c->G, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  if (c->cfg.token_pool && hipMemsetAsync(ws + c->off_pool, 0, c->ws_need - c->off_pool, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  if (hipStreamSynchronize(s) != hipSuccess) return AEP_ERR_DEVICE;
+  c->ws = ws;
+  c->device = devid;
+  c->num_cu = ncu > 0 ? ncu : 1;
+  for (auto& l : c->layers) {
+    l.clear();
+    l.cur = 0;
+    std::fill(l.have_w.begin(), l.have_w.end(), 0);
+  }
+  c->batch_out = false;
+  c->batch_expert = false;
+  std::fill(c->wtab_host.begin(), c->wtab_host.end(), WeightDesc{});
+  return AEP_OK;
+}
 
 // Tiling of the FFN launches: nt[6] = column tiles per row tile, index
 // stage * 3 + family (stage 0 gate/up, 1 down; family big, medium, small),
@@ -240,32 +272,10 @@ aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stre
   if (!c || !d_ws) return AEP_ERR_INVALID_ARG;
   if (reinterpret_cast<uintptr_t>(d_ws) & 255) return AEP_ERR_INVALID_ARG;
   if (bytes < c->ws_need) return AEP_ERR_CAPACITY;
-  if (c->batch_out) return AEP_ERR_STATE;
-  int devid = -1, ncu = 0;
+  if (c->batch_out && ws_bound(c)) return AEP_ERR_STATE;
+  int devid = -1;
   if (hipGetDevice(&devid) != hipSuccess) return AEP_ERR_DEVICE;
-  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, devid) != hipSuccess)
-    return AEP_ERR_DEVICE;
-  hipStream_t s = as_stream(stream);
-  char* ws = reinterpret_cast<char*>(d_ws);
-  // clear the error flag, every depth counter and the weight tables
-  if (hipMemsetAsync(ws + c->off_err, 0, c->off_q - c->off_err, s) != hipSuccess) return AEP_ERR_DEVICE;
-  if (hipMemsetAsync(ws + c->off_wtab, 0, sizeof(WeightDesc) * c->cfg.n_layers * c->G, s) != hipSuccess)
-    return AEP_ERR_DEVICE;
-  if (c->cfg.token_pool && hipMemsetAsync(ws + c->off_pool, 0, c->ws_need - c->off_pool, s) != hipSuccess)
-    return AEP_ERR_DEVICE;
-  if (hipStreamSynchronize(s) != hipSuccess) return AEP_ERR_DEVICE;
-  c->ws = ws;
-  c->device = devid;
-  c->num_cu = ncu > 0 ? ncu : 1;
-  for (auto& l : c->layers) {
-    l.clear();
-    l.cur = 0;
-    std::fill(l.have_w.begin(), l.have_w.end(), 0);
-  }
-  c->batch_out = false;
-  c->batch_expert = false;
-  std::fill(c->wtab_host.begin(), c->wtab_host.end(), WeightDesc{});
-  return AEP_OK;
+  return bind(c, reinterpret_cast<char*>(d_ws), devid, as_stream(stream));
 }
 
 aep_status aep_set_expert_weights(aep_ctx* ctx, int32_t layer, int32_t expert, const void* w_gate,
@@ -273,7 +283,7 @@ aep_status aep_set_expert_weights(aep_ctx* ctx, int32_t layer, int32_t expert, c
                                   const void* scale_down, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c) return AEP_ERR_INVALID_ARG;
-  if (!c->ws) return AEP_ERR_STATE;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   if (layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->G) return AEP_ERR_INVALID_ARG;
   if (!w_gate || !w_up || !w_down) return AEP_ERR_INVALID_ARG;
   const bool fp8 = c->cfg.w_dtype == AEP_FP8_E4M3;
@@ -296,7 +306,7 @@ aep_status aep_set_expert_weights(aep_ctx* ctx, int32_t layer, int32_t expert, c
 static aep_status route_common(Ctx* c, int32_t layer, const void* x, const float* logits, int32_t T,
                                const int32_t* token_ids, int32_t* idx_out, float* w_out, void* stream) {
   if (!c) return AEP_ERR_INVALID_ARG;
-  if (!c->ws) return AEP_ERR_STATE;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   if (layer < 0 || layer >= c->cfg.n_layers || T < 0) return AEP_ERR_INVALID_ARG;
   if (token_ids && !c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
   LayerState& L = c->layers[layer];
@@ -316,14 +326,13 @@ static aep_status route_common(Ctx* c, int32_t layer, const void* x, const float
   int32_t* rrank = c->at<int32_t>(c->off_rrank);
   int32_t* bcnt = c->at<int32_t>(c->off_blockcnt);
   hipError_t e1 = launch_route(logits, T, E, k, c->cfg.renorm, ridx, rw, rrank, bcnt, idx_out, w_out,
-                               c->err(), s);
+                               c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), c->route_done(), c->err(), s);
   if (e1 != hipSuccess) return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   hipError_t e2 = launch_append(ridx, rw, rrank, bcnt, T, E, k, reinterpret_cast<const char*>(x), row_bytes,
-                                want_pool ? 0 : L.tokens, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1),
-                                c->q(layer), c->tmax(), c->tokrow(layer), token_ids, (int)c->tmax(),
-                                want_pool ? c->live(layer) : nullptr, want_pool ? c->pend(layer) : nullptr,
-                                c->err(), s);
+                                want_pool ? 0 : L.tokens, c->q(layer), c->tmax(), c->tokrow(layer), token_ids,
+                                (int)c->tmax(), want_pool ? c->live(layer) : nullptr,
+                                want_pool ? c->pend(layer) : nullptr, c->err(), s);
   if (e2 != hipSuccess) return AEP_ERR_DEVICE;
   L.cur ^= 1;
   if (!want_pool) L.tokens += T;
@@ -352,7 +361,7 @@ aep_status aep_enqueue_rows(aep_ctx* ctx, int32_t layer, int32_t expert, const v
                             int32_t n, int32_t n_tokens, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c) return AEP_ERR_INVALID_ARG;
-  if (!c->ws) return AEP_ERR_STATE;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   if (layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->cfg.n_experts || n < 0)
     return AEP_ERR_INVALID_ARG;
   if (c->cfg.n_shared > 0) return AEP_ERR_UNSUPPORTED;
@@ -388,7 +397,7 @@ aep_status aep_queue_depth(const aep_ctx* ctx, int32_t layer, int64_t* tokens, i
 aep_status aep_expert_counts(aep_ctx* ctx, int32_t layer, int32_t* h_counts, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || !h_counts || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
-  if (!c->ws) return AEP_ERR_STATE;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   hipStream_t s = as_stream(stream);
   if (hipMemcpyAsync(h_counts, c->depth(layer, c->layers[layer].cur), sizeof(int32_t) * c->cfg.n_experts,
                      hipMemcpyDeviceToHost, s) != hipSuccess)
@@ -414,7 +423,7 @@ aep_status aep_pick_layer(const aep_ctx* ctx, int32_t policy, double delta, int3
 aep_status aep_rebatch(aep_ctx* ctx, int32_t layer, aep_batch* out, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c || !out || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
-  if (!c->ws || c->batch_out) return AEP_ERR_STATE;
+  if (!ws_bound(c) || c->batch_out) return AEP_ERR_STATE;
   LayerState& L = c->layers[layer];
   if (L.rows > 0 && L.pool) return AEP_ERR_STATE;  // pool-mode layers drain one expert at a time
   if (L.rows == 0 && !(c->cfg.n_shared > 0 && L.tokens > 0)) return AEP_ERR_EMPTY;
@@ -462,7 +471,7 @@ aep_status aep_rebatch_expert(aep_ctx* ctx, int32_t layer, int32_t expert, aep_b
   if (!c || !out || layer < 0 || layer >= c->cfg.n_layers || expert < 0 || expert >= c->cfg.n_experts)
     return AEP_ERR_INVALID_ARG;
   if (!c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
-  if (!c->ws || c->batch_out) return AEP_ERR_STATE;
+  if (!ws_bound(c) || c->batch_out) return AEP_ERR_STATE;
   LayerState& L = c->layers[layer];
   if (L.rows > 0 && !L.pool) return AEP_ERR_STATE;
   const int64_t nb = std::min(L.bound[expert], L.rows);
@@ -510,6 +519,7 @@ aep_status aep_rebatch_expert(aep_ctx* ctx, int32_t layer, int32_t expert, aep_b
 
 static aep_status check_batch(const Ctx* c, const aep_batch* b) {
   if (!c || !b) return AEP_ERR_INVALID_ARG;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   if (!c->batch_out || b->epoch != c->epoch || b->layer != c->batch_layer) return AEP_ERR_STATE;
   return AEP_OK;
 }
@@ -584,7 +594,7 @@ aep_status aep_pool_release(aep_ctx* ctx, int32_t layer, void* out, int32_t* rea
   Ctx* c = as_ctx(ctx);
   if (!c || layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
   if (!c->cfg.token_pool) return AEP_ERR_UNSUPPORTED;
-  if (!c->ws) return AEP_ERR_STATE;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   if (!out) return AEP_ERR_INVALID_ARG;
   return dev(launch_pool_release(c->cfg.act_dtype, c->pool(layer), c->live(layer), c->pend(layer),
                                  (int)c->tmax(), out, ready, c->cfg.d_model, as_stream(stream)));
@@ -604,7 +614,7 @@ aep_status aep_release_batch(aep_ctx* ctx, aep_batch* batch) {
 aep_status aep_sync(aep_ctx* ctx, void* stream) {
   Ctx* c = as_ctx(ctx);
   if (!c) return AEP_ERR_INVALID_ARG;
-  if (!c->ws) return AEP_ERR_STATE;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
   if (hipStreamSynchronize(as_stream(stream)) != hipSuccess) return AEP_ERR_DEVICE;
   int32_t flag = 0;
   if (hipMemcpy(&flag, c->err(), sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess) return AEP_ERR_DEVICE;

@@ -8,15 +8,17 @@
 // The softmax weights of the selected experts follow; lane j keeps slot j.
 // Each (token, slot) is then ranked among the workgroup's rows bound for the
 // same expert: one thread per expert walks the 32 tokens' selection masks in
-// token order.  Per-workgroup expert counts go to `blockcnt`.
+// token order.  Per-workgroup expert counts go to `blockcnt`; the workgroup
+// that finishes last (a counter, reset by that workgroup) rewrites them, per
+// expert, into each workgroup's first queue slot -- the current depth plus an
+// exclusive scan over the workgroups -- and publishes the new depths into the
+// other half of the layer's depth ping-pong buffer (the host flips halves
+// after the launch).  The scan reads every count once: linear in T.
 //
-// append: the same 32-token workgroups.  Every workgroup adds the counts of
-// the workgroups before it (and the queue's current depth) to get stable
-// global positions, then lane j of each token writes the queue entry of slot
-// j -- the order is exactly (fragment, token, slot) within each expert's
-// queue, with no atomics.  The last workgroup publishes the new depths into
-// the other half of the layer's depth ping-pong buffer; the host flips
-// halves after the launch.
+// append: the same 32-token workgroups.  Lane j of each token writes the
+// queue entry of slot j at its workgroup's first slot for that expert plus
+// its rank -- the order is exactly (fragment, token, slot) within each
+// expert's queue, with no atomics on the entries.
 #include <float.h>
 #include <limits.h>
 
@@ -27,11 +29,59 @@ namespace aep {
 static_assert(kMaxTopK <= kRouteLanes, "one slot per lane of a token");
 static_assert(kMaxRouteExperts <= kRouteThreads, "one thread per expert in the rank walk");
 
+// Per expert e, over workgroups b < nb of one router launch: blockcnt[b][e]
+// (rows of workgroup b bound for e) becomes depth_cur[e] + sum_{b' < b}
+// blockcnt[b'][e], the first queue slot of workgroup b's rows, and
+// depth_nxt[e] = depth_cur[e] + sum_b blockcnt[b][e].  One workgroup:
+// P = 256 / ES threads per expert (ES = E rounded up to a power of two)
+// each own a contiguous run of workgroups; a first pass sums the runs, the
+// run totals are scanned in LDS, a second pass writes the prefixes.  Counts
+// written by other workgroups of the launch are visible after the acquire
+// fence the caller issues before the scan (it invalidates this CU's vector
+// cache).
+__device__ void scan_counts(int32_t* blockcnt, int nb, int E, const int32_t* depth_cur, int32_t* depth_nxt) {
+  __shared__ int32_t run_sum[kRouteThreads];
+  const int tid = threadIdx.x;
+  int es = 1;
+  while (es < E) es <<= 1;
+  const int P = kRouteThreads / es;
+  const int e = tid % es, p = tid / es;
+  const int per = (nb + P - 1) / P;
+  const int b0 = min(nb, p * per), b1 = min(nb, b0 + per);
+  int acc = 0;
+  if (e < E)
+    for (int b = b0; b < b1; ++b)
+      acc += blockcnt[(int64_t)b * E + e];
+  run_sum[tid] = acc;
+  __syncthreads();
+  if (tid < E) {
+    // exclusive scan over the runs of expert tid, seeded with its depth
+    int x = depth_cur[tid];
+    for (int q = 0; q < P; ++q) {
+      const int v = run_sum[q * es + tid];
+      run_sum[q * es + tid] = x;
+      x += v;
+    }
+    depth_nxt[tid] = x;
+  }
+  __syncthreads();
+  if (e < E) {
+    int x = run_sum[tid];
+    for (int b = b0; b < b1; ++b) {
+      const int64_t i = (int64_t)b * E + e;
+      const int v = blockcnt[i];
+      blockcnt[i] = x;
+      x += v;
+    }
+  }
+}
+
 template <int EPL>
 __global__ __launch_bounds__(kRouteThreads) void route_count_kernel(
     const float* __restrict__ logits, int T, int E, int k, int renorm, int32_t* __restrict__ r_idx,
-    float* __restrict__ r_w, int32_t* __restrict__ r_rank, int32_t* __restrict__ blockcnt,
-    int32_t* __restrict__ idx_out, float* __restrict__ w_out, int32_t* __restrict__ err) {
+    float* __restrict__ r_w, int32_t* __restrict__ r_rank, int32_t* blockcnt,
+    int32_t* __restrict__ idx_out, float* __restrict__ w_out, const int32_t* __restrict__ depth_cur,
+    int32_t* __restrict__ depth_nxt, int32_t* done, int32_t* __restrict__ err) {
   __shared__ uint64_t sel_mask[kRouteTokens];
   __shared__ uint8_t rank_s[kRouteTokens][kMaxRouteExperts];
   const int tid = threadIdx.x, g = tid & (kRouteLanes - 1), tb = tid / kRouteLanes;
@@ -126,46 +176,28 @@ __global__ __launch_bounds__(kRouteThreads) void route_count_kernel(
     if (w_out) w_out[o] = w;
   }
   if (bad) atomicOr(err, kErrNonFinite);
+
+  // The last workgroup to finish scans every workgroup's counts.
+  __shared__ int last;
+  __threadfence();  // this workgroup's counts are visible device-wide
+  __syncthreads();
+  if (tid == 0) last = atomicAdd(done, 1) == (int)gridDim.x - 1;
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  scan_counts(blockcnt, (int)gridDim.x, E, depth_cur, depth_nxt);
+  if (tid == 0) *done = 0;  // ready for the next launch
 }
 
 __global__ __launch_bounds__(kRouteThreads) void append_kernel(
     const int32_t* __restrict__ r_idx, const float* __restrict__ r_w,
-    const int32_t* __restrict__ r_rank, const int32_t* __restrict__ blockcnt, int T, int E, int k,
-    const char* x, int64_t row_bytes, int32_t token_base, const int32_t* __restrict__ depth_cur,
-    int32_t* __restrict__ depth_nxt, QEntry* __restrict__ q, int64_t q_stride,
+    const int32_t* __restrict__ r_rank, const int32_t* __restrict__ first_slot, int T, int E, int k,
+    const char* x, int64_t row_bytes, int32_t token_base, QEntry* __restrict__ q, int64_t q_stride,
     const void** __restrict__ tok_row, const int32_t* __restrict__ token_ids, int n_ids,
     int32_t* __restrict__ live, int32_t* __restrict__ pend, int32_t* __restrict__ err) {
-  constexpr int kParts = kRouteThreads / kMaxRouteExperts;
-  __shared__ int32_t part[kParts][kMaxRouteExperts];
   __shared__ int32_t base[kMaxRouteExperts];
   const int tid = threadIdx.x;
-  {
-    // counts of the workgroups before this one, split over kParts threads
-    // per expert
-    const int e = tid % kMaxRouteExperts, p = tid / kMaxRouteExperts;
-    int acc = 0;
-    if (e < E) {
-      // 8 independent loads per round
-      int b = p;
-      for (; b + 7 * kParts < (int)blockIdx.x; b += 8 * kParts) {
-        int v[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = blockcnt[(int64_t)(b + i * kParts) * E + e];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc += v[i];
-      }
-      for (; b < (int)blockIdx.x; b += kParts) acc += blockcnt[(int64_t)b * E + e];
-    }
-    part[p][e] = acc;
-  }
-  __syncthreads();
-  if (tid < E) {
-    int acc = depth_cur[tid];
-#pragma unroll
-    for (int p = 0; p < kParts; ++p) acc += part[p][tid];
-    base[tid] = acc;
-    if (blockIdx.x == gridDim.x - 1) depth_nxt[tid] = acc + blockcnt[(int64_t)blockIdx.x * E + tid];
-  }
+  if (tid < E) base[tid] = first_slot[(int64_t)blockIdx.x * E + tid];
   __syncthreads();
   const int g = tid & (kRouteLanes - 1);
   const int t = blockIdx.x * kRouteTokens + tid / kRouteLanes;
@@ -227,33 +259,33 @@ __global__ __launch_bounds__(256) void enqueue_rows_kernel(
 
 hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,
                         float* r_w, int32_t* r_rank, int32_t* blockcnt, int32_t* idx_out,
-                        float* w_out, int32_t* err, hipStream_t s) {
+                        float* w_out, const int32_t* depth_cur, int32_t* depth_nxt, int32_t* done,
+                        int32_t* err, hipStream_t s) {
   const int nb = (T + kRouteTokens - 1) / kRouteTokens;
   if (E <= 8)
     route_count_kernel<1><<<nb, kRouteThreads, 0, s>>>(logits, T, E, k, renorm, r_idx, r_w, r_rank,
-                                                        blockcnt, idx_out, w_out, err);
+                                                        blockcnt, idx_out, w_out, depth_cur, depth_nxt, done, err);
   else if (E <= 16)
     route_count_kernel<2><<<nb, kRouteThreads, 0, s>>>(logits, T, E, k, renorm, r_idx, r_w, r_rank,
-                                                        blockcnt, idx_out, w_out, err);
+                                                        blockcnt, idx_out, w_out, depth_cur, depth_nxt, done, err);
   else if (E <= 32)
     route_count_kernel<4><<<nb, kRouteThreads, 0, s>>>(logits, T, E, k, renorm, r_idx, r_w, r_rank,
-                                                        blockcnt, idx_out, w_out, err);
+                                                        blockcnt, idx_out, w_out, depth_cur, depth_nxt, done, err);
   else
     route_count_kernel<8><<<nb, kRouteThreads, 0, s>>>(logits, T, E, k, renorm, r_idx, r_w, r_rank,
-                                                        blockcnt, idx_out, w_out, err);
+                                                        blockcnt, idx_out, w_out, depth_cur, depth_nxt, done, err);
   return hipGetLastError();
 }
 
 hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* r_rank,
-                         const int32_t* blockcnt, int T, int E, int k, const char* x,
-                         int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
-                         int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
-                         const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
-                         int32_t* err, hipStream_t s) {
+                         const int32_t* first_slot, int T, int E, int k, const char* x,
+                         int64_t row_bytes, int32_t token_base, QEntry* q, int64_t q_stride,
+                         const void** tok_row, const int32_t* token_ids, int n_ids, int32_t* live,
+                         int32_t* pend, int32_t* err, hipStream_t s) {
   const int nb = (T + kRouteTokens - 1) / kRouteTokens;
-  append_kernel<<<nb, kRouteThreads, 0, s>>>(r_idx, r_w, r_rank, blockcnt, T, E, k, x, row_bytes,
-                                              token_base, depth_cur, depth_nxt, q, q_stride, tok_row,
-                                              token_ids, n_ids, live, pend, err);
+  append_kernel<<<nb, kRouteThreads, 0, s>>>(r_idx, r_w, r_rank, first_slot, T, E, k, x, row_bytes,
+                                              token_base, q, q_stride, tok_row, token_ids, n_ids, live,
+                                              pend, err);
   return hipGetLastError();
 }
 

@@ -3,14 +3,15 @@ combine, release) captured in a HIP graph replays bit-identically: none of
 these calls synchronises or records a memset node, and the host-side queue
 state returns to where it started after one step.  Replays alternate with
 eager steps and host synchronisations, and every replay is checked against
-the eager result."""
+the eager result and against the oracle's layer (per-element tolerance)."""
 
 import numpy as np
 import pytest
 import torch
 
+import oracle
 import synth
-from gpu_helpers import log, make_context, to_dev, upload_weights
+from gpu_helpers import BF16_RTOL, assert_close, log, make_context, to_dev, to_host, upload_weights
 
 pytestmark = pytest.mark.gpu
 
@@ -45,6 +46,11 @@ def test_layer_step_graph_replays_match_eager(name):
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     ref = out.clone()
+    lq = oracle.LayerQueues(w.E, w.k, w.S, w.renorm)
+    for f in frags:
+        lq.enqueue_routed(f["x"], f["logits"])
+    want = oracle.moe_layer(lq, ws, w.act, w.wdt)["out"]
+    assert_close(oracle.act_to_f64(to_host(ref), w.act), want, BF16_RTOL, f"{name} eager step")
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         step()
@@ -54,10 +60,11 @@ def test_layer_step_graph_replays_match_eager(name):
         graph.replay()
         torch.cuda.synchronize()
         assert torch.equal(out, ref), f"replay {i}"
+        assert_close(oracle.act_to_f64(to_host(out), w.act), want, BF16_RTOL, f"{name} replay {i}")
         out.fill_(0)
         step()                      # eager work between replays
         torch.cuda.synchronize()
         assert torch.equal(out, ref), f"eager step after replay {i}"
     ctx.sync()
-    log(f"case {name}: 4 graph replays and 4 eager steps bit-identical")
+    log(f"case {name}: 4 graph replays and 4 eager steps bit-identical, and within tolerance of the oracle")
     del graph, ctx, dev

@@ -2,10 +2,13 @@
 times (fragments routed into the mu-queues, re-batch, gate/up + down, combine).
 
 Routing, counts, offsets, row order, (token, slot) positions and the gathered
-rows are compared bit-exactly with the oracle over the whole layer.  Outputs
-are compared on sampled tokens, which the oracle evaluates one by one with the
-dense brute force (every expert on the token, masked by its routing), and by
-properties that hold at any size (drain-order invariance, determinism).
+rows are compared bit-exactly with the oracle over the whole layer.  Every
+element of the expert outputs y and of the combined output is compared with
+the oracle's float64 layer (per element |g - r| <= atol + rtol |r|, and the
+normwise error ||g - r|| / ||r|| <= NORMWISE), and sampled tokens are checked
+once more against the dense brute force (every expert on the token, masked by
+its routing), which shares none of the oracle's queue code.  The 8-layer
+drain adds drain-order invariance and every layer's outputs element-wise.
 """
 
 import gc
@@ -20,6 +23,11 @@ from gpu_helpers import (BF16_RTOL, assert_close, check_routing_and_queues, log,
                          oracle_routed_layer, run_routed_layer, to_dev, to_host, upload_weights)
 
 pytestmark = pytest.mark.gpu
+
+# normwise bound for the bf16 / fp8-weight layers: h, y and out are each
+# rounded to bf16 once (2^-9 relative each, partly cancelling in the sums);
+# measured 2.9e-3 on the Mixtral-style layer
+NORMWISE = 5e-3
 
 
 def _free():
@@ -49,6 +57,12 @@ def _check_sampled(w, frags, ws, got_out, ref_batch, n=48):
                         f"{w.name}: {len(toks)} sampled tokens")
 
 
+def _check_all(got, ref, what, act="bf16"):
+    st = assert_close(oracle.act_to_f64(got, act), ref, BF16_RTOL, what)
+    assert st["normwise"] <= NORMWISE, (what, st)
+    return st
+
+
 @pytest.mark.parametrize("name", ["c2", "c3"])
 def test_full_routed_layer(name):
     w = synth.workload(name)
@@ -58,15 +72,17 @@ def test_full_routed_layer(name):
     ctx = make_context(w)
     dev = upload_weights(ctx, w, 0, ws)
     got = run_routed_layer(ctx, w, 0, frags)
-    log(f"case {name}: GPU done, counts {got['counts'].tolist()}")
-    ref = oracle_routed_layer(w, frags, ws, full_ffn=False)
-    check_routing_and_queues(w, got, ref)
-    log(f"case {name}: routing/queues/gather bit-exact")
-    st = _check_sampled(w, frags, ws, got["out"], ref["batch"])
-    log(f"case {name}: sampled outputs {st}")
-    assert np.all(np.isfinite(oracle.act_to_f64(got["out"], w.act)))
     del ctx, dev
     _free()
+    log(f"case {name}: GPU done, counts {got['counts'].tolist()}")
+    ref = oracle_routed_layer(w, frags, ws, full_ffn=True)
+    check_routing_and_queues(w, got, ref)
+    log(f"case {name}: routing/queues/gather bit-exact")
+    sy = _check_all(got["y"], ref["y"], f"{name} y, every element")
+    so = _check_all(got["out"], ref["out"], f"{name} out, every element")
+    log(f"case {name}: y {sy}; out {so}")
+    st = _check_sampled(w, frags, ws, got["out"], ref["batch"])
+    log(f"case {name}: sampled against the dense brute force {st}")
 
 
 @pytest.mark.parametrize("name", ["c4", "c4fp8"])
@@ -89,43 +105,42 @@ def test_full_rows_layer(name):
     b = ctx.rebatch(0)
     y = ctx.expert_ffn(b)
     out = ctx.combine(b, y)
-    ref_b = oracle.rebatch(lq)
-    ref_xp = oracle.gather(ref_b)
-    assert np.array_equal(to_host(b.counts()), ref_b.counts)
-    assert np.array_equal(to_host(b.offsets()), ref_b.offsets.astype(np.int32))
-    assert np.array_equal(to_host(b.row_token()), ref_b.row_token)
-    assert np.array_equal(to_host(b.token_pos()), ref_b.pos)
-    assert np.array_equal(to_host(b.x_perm()), ref_xp)
+    got = {k: to_host(v) for k, v in (("counts", b.counts()), ("offsets", b.offsets()), ("row_token", b.row_token()),
+                                       ("pos", b.token_pos()), ("xp", b.x_perm()), ("y", y), ("out", out))}
+    ctx.release(b)
+    ctx.sync()
+    del ctx, dev, keep, y, out
+    _free()
+    ref = oracle.moe_layer(lq, ws, w.act, w.wdt)
+    rb = ref["batch"]
+    assert np.array_equal(got["counts"], rb.counts)
+    assert np.array_equal(got["offsets"], rb.offsets.astype(np.int32))
+    assert np.array_equal(got["row_token"], rb.row_token)
+    assert np.array_equal(got["pos"], rb.pos)
+    assert np.array_equal(got["xp"], ref["xp"])
     log(f"case {name}: queues/gather bit-exact, depths {rw['depths'].tolist()}")
-    # sampled rows of every expert: first, last and a few in between
-    yh, oh = to_host(y), to_host(out)
+    sy = _check_all(got["y"], ref["y"], f"{name} y, every element")
+    so = _check_all(got["out"], ref["out"], f"{name} out, every element")
+    log(f"case {name}: y {sy}; out {so}")
+    # the dense definition on a few rows of every expert (no queues involved)
     rows = []
     for e in range(w.E):
-        o, n = int(ref_b.offsets[e]), int(ref_b.counts[e])
+        o, n = int(rb.offsets[e]), int(rb.counts[e])
         rows += sorted(set([o, o + n - 1] + [o + (n * q) // 5 for q in range(1, 5)]))
     rows = np.array(rows)
     ref_y = np.zeros((len(rows), w.d))
     for e in range(w.E):
-        m = (rows >= ref_b.offsets[e]) & (rows < ref_b.offsets[e + 1])
+        m = (rows >= rb.offsets[e]) & (rows < rb.offsets[e + 1])
         if m.any():
-            ref_y[m] = oracle.swiglu(oracle.bf16_to_f64(ref_xp[rows[m]]), *oracle.weights_to_f64(ws[e], w.wdt))
-    sy = assert_close(oracle.bf16_to_f64(yh[rows]), ref_y, BF16_RTOL, f"{name} sampled y rows")
-    toks = ref_b.row_token[rows]
-    ref_out = ref_b.row_w[rows].astype(np.float64)[:, None] * ref_y
-    so = assert_close(oracle.bf16_to_f64(oh[toks]), ref_out, BF16_RTOL, f"{name} sampled out rows")
-    log(f"case {name}: y {sy} out {so}")
-    ctx.release(b)
-    ctx.sync()
-    del ctx, dev, keep
-    _free()
+            ref_y[m] = oracle.swiglu(oracle.bf16_to_f64(ref["xp"][rows[m]]), *oracle.weights_to_f64(ws[e], w.wdt))
+    assert_close(oracle.bf16_to_f64(got["y"][rows]), ref_y, BF16_RTOL, f"{name} sampled y rows (dense)")
 
 
-def test_c5_multi_layer_drain():
-    """Eight layers queued at once (0..8192 tokens each, 32768 in total); the
-    most-tokens-first policy drains them one by one.  Checks: the pick order,
-    per-layer queues bit-exact, sampled outputs on three layers against the
-    dense brute force, and bit-identical layer outputs when the same queues
-    are drained in the opposite order."""
+@pytest.fixture(scope="module")
+def c5_drain():
+    """Eight layers queued at once (0..8192 tokens each, 32768 in total),
+    drained most-tokens-first, then refilled and drained in the opposite
+    order.  Returns the host copies every check below needs."""
     w = synth.workload("c5")
     log(f"case c5: layer tokens {w.tokens}")
     base = synth.all_expert_weights(synth.workload("c2"), 0, threads=16)  # rotated per layer
@@ -159,38 +174,54 @@ def test_c5_multi_layer_drain():
 
     fill()
     rows = [ctx.queue_depth(l)[1] for l in range(w.n_layers)]
-    assert rows == [2 * t for t in w.tokens]
-    gpu_counts = [ctx.expert_counts(l) for l in range(w.n_layers)]
+    counts = [ctx.expert_counts(l) for l in range(w.n_layers)]
     outs, order = drain(lambda: ctx.pick_layer("mtfs"))
-    remaining, expect = [2 * t for t in w.tokens], []
+    log(f"case c5: MTFS drain order {order}")
+    fill()
+    outs2, order2 = drain(lambda: max([l for l in range(w.n_layers) if ctx.queue_depth(l)[1] > 0], default=None))
+    del ctx, wdev, base_dev, dev_frags
+    _free()
+    return dict(w=w, base=base, frags=frags, rows=rows, counts=counts, outs=outs, order=order, outs2=outs2,
+                order2=order2)
+
+
+def test_c5_drain_order_and_queues(c5_drain):
+    d = c5_drain
+    w = d["w"]
+    assert d["rows"] == [2 * t for t in w.tokens]
+    remaining, expect = list(d["rows"]), []
     while (nxt := oracle.pick_mtfs(remaining)) is not None:
         expect.append(nxt)
         remaining[nxt] = 0
-    assert order == expect
-    log(f"case c5: MTFS drain order {order}")
-    # reverse drain order: identical per-layer outputs, bit for bit
-    fill()
-    outs2, order2 = drain(lambda: max([l for l in range(w.n_layers) if ctx.queue_depth(l)[1] > 0], default=None))
-    assert order2 == sorted(order, reverse=True)
-    for l in order:
-        assert np.array_equal(outs[l], outs2[l]), f"layer {l} differs between drain orders"
-    log("case c5: drain-order invariance bit-exact")
-    # oracle: per-expert queue depths of every layer bit-exact; sampled
-    # outputs on 3 layers
+    assert d["order"] == expect
+    assert d["order2"] == sorted(d["order"], reverse=True)
+    for l in d["order"]:
+        assert np.array_equal(d["outs"][l], d["outs2"][l]), f"layer {l} differs between drain orders"
+    log("case c5: MTFS order, drain-order invariance bit-exact")
     for l in range(w.n_layers):
         lq = oracle.LayerQueues(w.E, w.k)
-        for fr in frags[l]:
+        for fr in d["frags"][l]:
             lq.enqueue_routed(fr["x"], fr["logits"])
-        b = oracle.rebatch(lq) if w.tokens[l] else None
-        ref_counts = b.counts if b is not None else np.zeros(w.E, np.int32)
-        assert np.array_equal(gpu_counts[l], ref_counts), (l, gpu_counts[l], ref_counts)
-    lws = lambda l: [base[synth.weight_source(w, l, e)[2]] for e in range(w.E)]
-    for l in order[:1] + order[len(order) // 2:len(order) // 2 + 1] + order[-1:]:
-        x = np.concatenate([f["x"] for f in frags[l]])
-        lg = np.concatenate([f["logits"] for f in frags[l]])
-        toks = np.unique(np.linspace(0, x.shape[0] - 1, 16).astype(int))
-        ref = oracle.brute_dense(x[toks], lg[toks], lws(l), w.k, w.renorm, 0, "bf16", "bf16")
-        st = assert_close(oracle.bf16_to_f64(outs[l][toks]), ref, BF16_RTOL, f"c5 layer {l} sampled")
-        log(f"case c5: layer {l} sampled {st}")
-    del ctx, wdev, base_dev
-    _free()
+        ref_counts = oracle.rebatch(lq).counts if w.tokens[l] else np.zeros(w.E, np.int32)
+        assert np.array_equal(d["counts"][l], ref_counts), (l, d["counts"][l], ref_counts)
+
+
+@pytest.mark.parametrize("layer", range(8))
+def test_c5_layer_every_element(c5_drain, layer):
+    d = c5_drain
+    w = d["w"]
+    if w.tokens[layer] == 0:
+        assert layer not in d["outs"]
+        pytest.skip("layer holds no tokens (never drained)")
+    lws = [d["base"][synth.weight_source(w, layer, e)[2]] for e in range(w.E)]
+    lq = oracle.LayerQueues(w.E, w.k)
+    for fr in d["frags"][layer]:
+        lq.enqueue_routed(fr["x"], fr["logits"])
+    ref = oracle.moe_layer(lq, lws, "bf16", "bf16")
+    st = _check_all(d["outs"][layer], ref["out"], f"c5 layer {layer} out, every element")
+    log(f"case c5: layer {layer} ({w.tokens[layer]} tokens) {st}")
+    x = np.concatenate([f["x"] for f in d["frags"][layer]])
+    lg = np.concatenate([f["logits"] for f in d["frags"][layer]])
+    toks = np.unique(np.linspace(0, x.shape[0] - 1, 16).astype(int))
+    bd = oracle.brute_dense(x[toks], lg[toks], lws, w.k, w.renorm, 0, "bf16", "bf16")
+    assert_close(oracle.bf16_to_f64(d["outs"][layer][toks]), bd, BF16_RTOL, f"c5 layer {layer} sampled (dense)")
