@@ -129,6 +129,24 @@ aep_status aep_workspace_size(const aep_ctx* ctx, size_t* bytes);
  * mu-queues, weight tables, the batch buffers and the FFN intermediate. */
 aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): bind the
+ * library's own static workspace instead of a caller allocation.  The array
+ * holds AEP_STATIC_WORKSPACE_BYTES (64 MiB) on every GPU the library runs on,
+ * comes with the code object and lives until the process ends; nothing is
+ * allocated or freed by this call.  Otherwise as aep_bind_workspace: on the
+ * current HIP device, initialised on `stream` (waits for it), every queue
+ * reset, weights to be registered again.  AEP_ERR_CAPACITY (nothing changed)
+ * if aep_workspace_size exceeds the maximum; AEP_ERR_STATE while a batch of
+ * this context is outstanding.  All contexts bound this way on one GPU share
+ * that GPU's array, which keeps what the last user left there: binding
+ * another context takes the array over, and the earlier context's later
+ * calls return AEP_ERR_STATE until it is bound again.  Work that two such
+ * contexts enqueue so that it overlaps on the GPU (before the takeover, or
+ * on different streams) races and corrupts both. */
+#define AEP_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+aep_status aep_bind_static_workspace(aep_ctx* ctx, void* stream);
+
 /* Register one expert's weights for a layer (pointers are borrowed and must
  * stay valid while the layer can run).  expert in [0, E) is routed; expert
  * in [E, E + n_shared) is shared expert expert - E.  Device pointers:

@@ -19,6 +19,7 @@ AEP_OK, AEP_ERR_INVALID_ARG, AEP_ERR_CAPACITY, AEP_ERR_EMPTY, AEP_ERR_STATE, AEP
     AEP_ERR_UNSUPPORTED = range(7)
 AEP_F32, AEP_BF16, AEP_FP8_E4M3 = range(3)
 AEP_POLICY_MTFS, AEP_POLICY_FLFS, AEP_POLICY_DEFRAG = range(3)
+AEP_STATIC_WORKSPACE_BYTES = 64 << 20   # include/aep.h
 
 STATUS_NAMES = {0: "AEP_OK", 1: "AEP_ERR_INVALID_ARG", 2: "AEP_ERR_CAPACITY", 3: "AEP_ERR_EMPTY",
                 4: "AEP_ERR_STATE", 5: "AEP_ERR_DEVICE", 6: "AEP_ERR_UNSUPPORTED"}
@@ -75,6 +76,7 @@ _SIG = {
     "aep_destroy": (ctypes.c_int, [_P]),
     "aep_workspace_size": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "aep_bind_workspace": (ctypes.c_int, [_P, _P, ctypes.c_size_t, _P]),
+    "aep_bind_static_workspace": (ctypes.c_int, [_P, _P]),
     "aep_set_expert_weights": (ctypes.c_int, [_P, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "aep_route_enqueue": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _P, _P, _P]),
     "aep_enqueue_rows": (ctypes.c_int, [_P, _I32, _I32, _P, _P, _P, _P, _I32, _I32, _P]),

@@ -53,6 +53,8 @@ class BatchView:
 
     def _view(self, ptr: int, dtype: torch.dtype, shape: Tuple[int, ...]) -> torch.Tensor:
         ws = self.ctx.workspace
+        if ws is None:
+            raise RuntimeError("batch views need a torch-allocated workspace (this context uses the static one)")
         off = ptr - ws.data_ptr()
         n = int(np.prod(shape)) if shape else 1
         nbytes = n * torch.empty((), dtype=dtype).element_size()
@@ -87,7 +89,8 @@ class Context:
 
     def __init__(self, n_layers: int, n_experts: int, d_model: int, d_ffn: int, top_k: int, *,
                  n_shared: int = 0, renorm: bool = True, act: str = "bf16", wdt: str = "bf16",
-                 max_tokens_per_layer: int, token_pool: bool = False, device: Optional[torch.device] = None):
+                 max_tokens_per_layer: int, token_pool: bool = False, device: Optional[torch.device] = None,
+                 static_workspace: bool = False):
         self.lib = L.lib()
         self.n_layers, self.n_experts, self.n_shared = n_layers, n_experts, n_shared
         self.d_model, self.d_ffn, self.top_k = d_model, d_ffn, top_k
@@ -104,13 +107,20 @@ class Context:
         L.check(self.lib.aep_workspace_size(self.h, ctypes.byref(nbytes)), "aep_workspace_size")
         dev = device or torch.device("cuda", torch.cuda.current_device())
         self.device = dev
-        # 256-byte alignment: over-allocate and slice
-        raw = torch.empty(nbytes.value + 256, dtype=torch.uint8, device=dev)
-        pad = (-raw.data_ptr()) % 256
-        self._raw = raw
-        self.workspace = raw[pad:pad + nbytes.value]
-        L.check(self.lib.aep_bind_workspace(self.h, self.workspace.data_ptr(), nbytes.value, _stream()),
-                "aep_bind_workspace")
+        if static_workspace:
+            # the library's own workspace: nothing is allocated here (batch
+            # internals then have no tensor views; outputs are caller tensors)
+            self._raw = self.workspace = None
+            with torch.cuda.device(dev):
+                L.check(self.lib.aep_bind_static_workspace(self.h, _stream()), "aep_bind_static_workspace")
+        else:
+            # 256-byte alignment: over-allocate and slice
+            raw = torch.empty(nbytes.value + 256, dtype=torch.uint8, device=dev)
+            pad = (-raw.data_ptr()) % 256
+            self._raw = raw
+            self.workspace = raw[pad:pad + nbytes.value]
+            L.check(self.lib.aep_bind_workspace(self.h, self.workspace.data_ptr(), nbytes.value, _stream()),
+                    "aep_bind_workspace")
         self.workspace_need = nbytes.value
         self._frag_refs: Dict[int, List[torch.Tensor]] = {l: [] for l in range(n_layers)}
         self._w_refs: Dict[Tuple[int, int], Tuple[torch.Tensor, ...]] = {}

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -49,6 +50,8 @@ struct aep_ctx {
   size_t off_pool = 0, off_live = 0, off_pend = 0;  // token pools (cfg.token_pool)
   size_t ws_need = 0;
   char* ws = nullptr;
+  bool ws_static = false;   // ws is the library's static workspace (aep_bind_static_workspace)
+  uint64_t static_gen = 0;  // ... bound in this generation of that device's binding
   int device = -1;
   int num_cu = 0;
   std::vector<LayerState> layers;
@@ -141,10 +144,34 @@ hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 aep_status dev(hipError_t e) { return e == hipSuccess ? AEP_OK : AEP_ERR_DEVICE; }
 
-// A workspace is bound.
-bool ws_bound(const Ctx* c) { return c->ws != nullptr; }
+// The workspace of aep_bind_static_workspace: one array per GPU, allocated
+// with the code object and held until the process ends.  In host code its
+// name is only a stand-in; its device address comes from hipGetSymbolAddress
+// (looked up once per device, with that device current) and is the only
+// handle host code ever passes on.
+static __device__ __align__(256) unsigned char scratch[AEP_STATIC_WORKSPACE_BYTES];
 
-// Initialise the caller's workspace ws on stream s and
+struct StaticScratch {
+  std::mutex mu;
+  std::vector<char*> ptr;     // per device: address of `scratch` there (nullptr: not looked up yet)
+  std::vector<uint64_t> gen;  // per device: incremented by every binding
+};
+StaticScratch& static_scratch() {
+  static StaticScratch s;
+  return s;
+}
+
+// A workspace is bound, and, if it is the static one, no other context has
+// bound it since.
+bool ws_bound(const Ctx* c) {
+  if (!c->ws) return false;
+  if (!c->ws_static) return true;
+  StaticScratch& s = static_scratch();
+  std::lock_guard<std::mutex> g(s.mu);
+  return (size_t)c->device < s.gen.size() && s.gen[c->device] == c->static_gen;
+}
+
+// Initialise ws (the caller's allocation or the static array) on stream s and
 // reset every queue of c.
 aep_status bind(Ctx* c, char* ws, int devid, hipStream_t s) {
   int ncu = 0;
@@ -158,6 +185,7 @@ aep_status bind(Ctx* c, char* ws, int devid, hipStream_t s) {
     return AEP_ERR_DEVICE;
   if (hipStreamSynchronize(s) != hipSuccess) return AEP_ERR_DEVICE;
   c->ws = ws;
+  c->ws_static = false;
   c->device = devid;
   c->num_cu = ncu > 0 ? ncu : 1;
   for (auto& l : c->layers) {
@@ -276,6 +304,36 @@ aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stre
   int devid = -1;
   if (hipGetDevice(&devid) != hipSuccess) return AEP_ERR_DEVICE;
   return bind(c, reinterpret_cast<char*>(d_ws), devid, as_stream(stream));
+}
+
+aep_status aep_bind_static_workspace(aep_ctx* ctx, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return AEP_ERR_INVALID_ARG;
+  if (c->ws_need > AEP_STATIC_WORKSPACE_BYTES) return AEP_ERR_CAPACITY;
+  if (c->batch_out && ws_bound(c)) return AEP_ERR_STATE;
+  int devid = -1;
+  if (hipGetDevice(&devid) != hipSuccess || devid < 0) return AEP_ERR_DEVICE;
+  StaticScratch& ss = static_scratch();
+  char* base = nullptr;
+  {
+    std::lock_guard<std::mutex> g(ss.mu);
+    if ((size_t)devid >= ss.ptr.size()) {
+      ss.ptr.resize((size_t)devid + 1, nullptr);
+      ss.gen.resize((size_t)devid + 1, 0);
+    }
+    if (!ss.ptr[devid]) {
+      void* p = nullptr;
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return AEP_ERR_DEVICE;
+      ss.ptr[devid] = reinterpret_cast<char*>(p);
+    }
+    base = ss.ptr[devid];
+  }
+  const aep_status st = bind(c, base, devid, as_stream(stream));
+  if (st != AEP_OK) return st;
+  std::lock_guard<std::mutex> g(ss.mu);
+  c->ws_static = true;
+  c->static_gen = ++ss.gen[devid];
+  return AEP_OK;
 }
 
 aep_status aep_set_expert_weights(aep_ctx* ctx, int32_t layer, int32_t expert, const void* w_gate,
