@@ -68,6 +68,7 @@ constexpr int kRouteThreads = 256;
 constexpr int kRouteLanes = 8;                              // lanes per token in the router
 constexpr int kRouteTokens = kRouteThreads / kRouteLanes;   // tokens per router workgroup
 constexpr int kMaxRouteExperts = 64;
+constexpr int kDirectPrefixBlocks = 64;  // router workgroups whose appends sum earlier counts directly
 constexpr int kMaxTopK = 8;
 constexpr int kMaxGroups = 1024;
 
@@ -93,10 +94,12 @@ bool pick_block(const int64_t* R, int nb, int policy, double delta, int lookahea
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipGetLastError() after the launch.
-// Routes T tokens; blockcnt [ceil(T / kRouteTokens)][E] receives the first
-// queue slot of each router workgroup's rows per expert and depth_nxt the new
-// depths (depth_cur + this fragment's counts).  done: a launch counter that
-// must be 0 before the launch (the kernel leaves it 0).
+// Routes T tokens; blockcnt [ceil(T / kRouteTokens)][E] receives each router
+// workgroup's row count per expert.  Above kDirectPrefixBlocks workgroups the
+// launch then rewrites them into each workgroup's first queue slot and writes
+// depth_nxt (depth_cur + this fragment's counts); below, append does both.
+// done: a launch counter that must be 0 before the launch (the kernel leaves
+// it 0).
 hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,
                         float* r_w, int32_t* r_rank, int32_t* blockcnt, int32_t* idx_out,
                         float* w_out, const int32_t* depth_cur, int32_t* depth_nxt, int32_t* done,
@@ -105,9 +108,10 @@ hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, in
 // id is token_ids[t] (< n_ids) and it claims pool entry live[id] / pend[id].
 hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* r_rank,
                          const int32_t* first_slot, int T, int E, int k, const char* x,
-                         int64_t row_bytes, int32_t token_base, QEntry* q, int64_t q_stride,
-                         const void** tok_row, const int32_t* token_ids, int n_ids, int32_t* live,
-                         int32_t* pend, int32_t* err, hipStream_t s);
+                         int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
+                         int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
+                         const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
+                         int32_t* err, hipStream_t s);
 hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_t* token_ids,
                                const int32_t* slots, const float* gate_w, int n, int n_tokens,
                                int k, int expert, int E, const int32_t* depth_cur,
@@ -122,10 +126,14 @@ hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_
 // 0 rows and keeps its queue).  depth is the current half of the layer's
 // depth ping-pong, depth_other the other one; both are cleared for the
 // drained experts.
+// tile_group [2][tile_cap]: the group of each tile of the gate/up (row 0) and
+// down (row 1) launch, tiles numbered big family first, then medium, small;
+// tile_cap bounds either launch's tile count.
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
                        int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
                        int32_t* tile_totals, const int* nt, int big_bm, int med_bm, int small_bm,
-                       int num_cu, int32_t* pos, float* posw, hipStream_t s);
+                       int num_cu, int32_t* tile_group, int64_t tile_cap, int32_t* pos, float* posw,
+                       hipStream_t s);
 // N bounds the routed rows (the exact count is offsets[E] on the device);
 // pos == nullptr skips the (token, slot) -> row map.
 hipError_t launch_gather(const QEntry* q, int64_t q_stride, const int32_t* offsets, int E,
@@ -140,11 +148,13 @@ hipError_t launch_pool_accumulate(int act_dtype, const void* y, int64_t N, const
 hipError_t launch_pool_release(int act_dtype, float* pool, int32_t* live, int32_t* pend, int n_ids,
                                void* out, int32_t* ready, int d, hipStream_t s);
 // stage 0: gate/up (xp -> h), stage 1: down (h -> y); max_tiles bounds the
-// stage's tile count (the exact count is on the device).
+// stage's tile count (the exact count is on the device); tile_group is that
+// stage's row of the plan's tile -> group map.
 // clk != nullptr: workgroup w < clk_n writes its elapsed (s_memtime,
 // s_memrealtime) ticks to clk[2w], clk[2w + 1] (bf16 / fp8 weights only).
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
-                      const WeightDesc* wtab, int G, const int32_t* tile_totals, int max_tiles,
+                      const WeightDesc* wtab, int G, const int32_t* tile_totals,
+                      const int32_t* tile_group, int max_tiles,
                       const void* xp, void* h, void* y, int d, int f, int num_cu,
                       unsigned long long* clk, int clk_n, hipStream_t s);
 hipError_t launch_combine(int act_dtype, const void* y, int64_t N, int n_tokens, int S, int k,

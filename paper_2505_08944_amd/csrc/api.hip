@@ -45,7 +45,8 @@ struct aep_ctx {
   // workspace layout (byte offsets)
   size_t off_err = 0, off_depth = 0, off_q = 0, off_tokrow = 0, off_wtab = 0;
   size_t off_ridx = 0, off_rw = 0, off_rrank = 0, off_blockcnt = 0;
-  size_t off_counts = 0, off_offsets = 0, off_groups = 0, off_tiles = 0;
+  size_t off_counts = 0, off_offsets = 0, off_groups = 0, off_tiles = 0, off_tilegrp = 0;
+  int64_t tile_cap = 0;  // entries per FFN launch in the tile -> group map
   size_t off_xp = 0, off_rowtok = 0, off_roww = 0, off_pos = 0, off_posw = 0, off_h = 0;
   size_t off_pool = 0, off_live = 0, off_pend = 0;  // token pools (cfg.token_pool)
   size_t ws_need = 0;
@@ -95,6 +96,43 @@ namespace {
 
 using Ctx = aep_ctx;
 
+// Tiling of the FFN launches: nt[6] = column tiles per row tile, index
+// stage * 3 + family (stage 0 gate/up, 1 down; family big, medium, small),
+// and the row-tile heights.  f32 uses 64 x 64 tiles only; bf16 and fp8
+// weights use 256 x 256 big tiles, 128 x 128 medium and 64 x 128 small ones.
+void tiling(const Ctx& c, int nt[6], int* big_bm, int* med_bm, int* small_bm) {
+  const int d = c.cfg.d_model, f = c.cfg.d_ffn;
+  auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
+  if (c.cfg.act_dtype == AEP_F32) {
+    nt[0] = nt[1] = nt[2] = cdiv(f, kBN32);
+    nt[3] = nt[4] = nt[5] = cdiv(d, kBN32);
+    *big_bm = kBM32;
+    *med_bm = *small_bm = 0;
+  } else {
+    nt[0] = cdiv(f, kBN / 2);
+    nt[1] = cdiv(f, kMedBN / 2);
+    nt[2] = cdiv(f, kSmallBN / 2);
+    nt[3] = cdiv(d, kBN);
+    nt[4] = cdiv(d, kMedBN);
+    nt[5] = cdiv(d, kSmallBN);
+    *big_bm = kBM;
+    *med_bm = kMedBM;
+    *small_bm = kSmallBM;
+  }
+}
+
+// Upper bound of one FFN launch's tiles for a batch of N routed rows and T
+// tokens: every group's rows in big tiles (one partial big row tile per
+// non-empty group), plus at most 2 medium and 1 small row tiles per group.
+int64_t tile_bound(const Ctx& c, int stage, int64_t N, int64_t T) {
+  int nt[6], big_bm, med_bm, small_bm;
+  tiling(c, nt, &big_bm, &med_bm, &small_bm);
+  const int64_t E = c.cfg.n_experts, S = c.cfg.n_shared, G = E + S;
+  const int64_t big_rows = N / big_bm + std::min<int64_t>(E, N) + S * ((T + big_bm - 1) / big_bm);
+  const int* ns = nt + 3 * stage;
+  return big_rows * ns[0] + (small_bm ? G * (2 * (int64_t)ns[1] + ns[2]) : 0);
+}
+
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 bool layout(Ctx& c) {
@@ -123,6 +161,8 @@ bool layout(Ctx& c) {
   c.off_offsets = take(sizeof(int32_t) * (c.G + 1));
   c.off_groups = take(sizeof(GroupDesc) * c.G);
   c.off_tiles = take(sizeof(int32_t) * 6);
+  c.tile_cap = std::max(tile_bound(c, 0, N, T), tile_bound(c, 1, N, T));
+  c.off_tilegrp = take(sizeof(int32_t) * 2 * c.tile_cap);
   c.off_xp = take((size_t)xrows * d * c.esz);
   c.off_rowtok = take(sizeof(int32_t) * N);
   c.off_roww = take(sizeof(float) * N);
@@ -199,30 +239,6 @@ aep_status bind(Ctx* c, char* ws, int devid, hipStream_t s) {
   return AEP_OK;
 }
 
-// Tiling of the FFN launches: nt[6] = column tiles per row tile, index
-// stage * 3 + family (stage 0 gate/up, 1 down; family big, medium, small),
-// and the row-tile heights.  f32 uses 64 x 64 tiles only; bf16 and fp8
-// weights use 256 x 256 big tiles, 128 x 128 medium and 64 x 128 small ones.
-void tiling(const Ctx& c, int nt[6], int* big_bm, int* med_bm, int* small_bm) {
-  const int d = c.cfg.d_model, f = c.cfg.d_ffn;
-  auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
-  if (c.cfg.act_dtype == AEP_F32) {
-    nt[0] = nt[1] = nt[2] = cdiv(f, kBN32);
-    nt[3] = nt[4] = nt[5] = cdiv(d, kBN32);
-    *big_bm = kBM32;
-    *med_bm = *small_bm = 0;
-  } else {
-    nt[0] = cdiv(f, kBN / 2);
-    nt[1] = cdiv(f, kMedBN / 2);
-    nt[2] = cdiv(f, kSmallBN / 2);
-    nt[3] = cdiv(d, kBN);
-    nt[4] = cdiv(d, kMedBN);
-    nt[5] = cdiv(d, kSmallBN);
-    *big_bm = kBM;
-    *med_bm = kMedBM;
-    *small_bm = kSmallBM;
-  }
-}
 
 }  // namespace
 
@@ -388,7 +404,8 @@ static aep_status route_common(Ctx* c, int32_t layer, const void* x, const float
   if (e1 != hipSuccess) return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   hipError_t e2 = launch_append(ridx, rw, rrank, bcnt, T, E, k, reinterpret_cast<const char*>(x), row_bytes,
-                                want_pool ? 0 : L.tokens, c->q(layer), c->tmax(), c->tokrow(layer), token_ids,
+                                want_pool ? 0 : L.tokens, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1),
+                                c->q(layer), c->tmax(), c->tokrow(layer), token_ids,
                                 (int)c->tmax(), want_pool ? c->live(layer) : nullptr,
                                 want_pool ? c->pend(layer) : nullptr, c->err(), s);
   if (e2 != hipSuccess) return AEP_ERR_DEVICE;
@@ -497,7 +514,7 @@ aep_status aep_rebatch(aep_ctx* ctx, int32_t layer, aep_batch* out, void* stream
   float* posw = c->at<float>(c->off_posw);
   if (launch_plan(E, S, L.tokens, k, -1, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
                   c->at<GroupDesc>(c->off_groups), c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm,
-                  small_bm, c->num_cu, pos, posw, s) != hipSuccess)
+                  small_bm, c->num_cu, c->at<int32_t>(c->off_tilegrp), c->tile_cap, pos, posw, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, L.rows, L.tokens, S > 0, c->tokrow(layer),
@@ -543,8 +560,8 @@ aep_status aep_rebatch_expert(aep_ctx* ctx, int32_t layer, int32_t expert, aep_b
   int32_t* offsets = c->at<int32_t>(c->off_offsets);
   if (launch_plan(E, 0, 0, k, expert, c->depth(layer, L.cur), c->depth(layer, L.cur ^ 1), counts, offsets,
                   c->at<GroupDesc>(c->off_groups),
-                  c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm, small_bm, c->num_cu, nullptr, nullptr,
-                  s) != hipSuccess)
+                  c->at<int32_t>(c->off_tiles), nt, big_bm, med_bm, small_bm, c->num_cu,
+                  c->at<int32_t>(c->off_tilegrp), c->tile_cap, nullptr, nullptr, s) != hipSuccess)
     return AEP_ERR_DEVICE;
   const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
   if (launch_gather(c->q(layer), c->tmax(), offsets, E, nb, 0, 0, c->tokrow(layer), c->at<char>(c->off_xp),
@@ -586,18 +603,11 @@ static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, 
   aep_status st = check_batch(c, batch);
   if (st != AEP_OK) return st;
   if (stage == 1 && !y) return AEP_ERR_INVALID_ARG;
-  int nt[6], big_bm, med_bm, small_bm;
-  tiling(*c, nt, &big_bm, &med_bm, &small_bm);
-  const int64_t E = c->cfg.n_experts, S = c->cfg.n_shared, G = E + S;
-  const int64_t N = batch->n_routed, T = batch->n_tokens;
-  // bound on tiles: every group's rows in big tiles, plus at most 2 medium
-  // and 1 small row tiles per group
-  const int64_t big_rows = N / big_bm + std::min<int64_t>(E, N) + S * ((T + big_bm - 1) / big_bm);
-  const int* ns = nt + 3 * stage;
-  const int64_t mt = big_rows * ns[0] + (small_bm ? G * (2 * (int64_t)ns[1] + ns[2]) : 0);
-  if (mt > INT32_MAX) return AEP_ERR_UNSUPPORTED;
+  const int64_t mt = tile_bound(*c, stage, batch->n_routed, batch->n_tokens);
+  if (mt > INT32_MAX || mt > c->tile_cap) return AEP_ERR_UNSUPPORTED;
   return dev(launch_ffn(stage, c->cfg.act_dtype, c->cfg.w_dtype, c->at<GroupDesc>(c->off_groups),
-                        c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles), (int)mt,
+                        c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles),
+                        c->at<int32_t>(c->off_tilegrp) + stage * c->tile_cap, (int)mt,
                         c->ws + c->off_xp, c->ws + c->off_h, y, c->cfg.d_model, c->cfg.d_ffn, c->num_cu,
                         c->clk, c->clk_n, as_stream(stream)));
 }

@@ -46,6 +46,7 @@ struct FfnParams {
   const GroupDesc* groups;
   const WeightDesc* wtab;
   const int32_t* tile_totals;
+  const int32_t* tile_group;  // group of each tile of this launch (written by the plan)
   const void* a;  // x_perm (gate/up) or h (down)
   void* out;      // h (gate/up) or y (down)
   int G;
@@ -78,18 +79,6 @@ __device__ __forceinline__ void panel_decode(int local, int nrow, int ncol, int&
   const int w = min(PANEL, ncol - pi * PANEL);  // the last panel may be narrower
   rt = within / w;
   ct = pi * PANEL + (within - rt * w);
-}
-
-__device__ __forceinline__ int find_group(const int32_t* t0s, int G, int tile) {
-  int lo = 0, hi = G;  // t0s[lo] <= tile < t0s[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (t0s[mid] <= tile)
-      lo = mid;
-    else
-      hi = mid;
-  }
-  return lo;
 }
 
 // ------------------------------------------------- direct-to-LDS MFMA tiles
@@ -168,9 +157,10 @@ __device__ __forceinline__ void wait_steps(int per) {
 // same assignment of k to lanes (bf16 chunks 4m + 2h and 4m + 2h + 1 for
 // lane half h), so every MFMA still pairs equal k; per-channel scales are
 // applied in the epilogue.
-template <bool GATED, bool FP8, int BM, int BN, int STAGES, int CAP>
+template <bool GATED, bool FP8, int BM, int BN, int STAGES, int BSTAGES, int CAP>
 __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem, uint32_t lds_base,
-                                        const GroupDesc& gd, const WeightDesc& wd, int nti, int m0) {
+                                        const GroupDesc& gd, const WeightDesc& wd, int nti, int m0,
+                                        int rot_seed) {
   constexpr int BKS = kBK;
   constexpr int kRowA = BKS * 2;              // 128 bytes: one A row of one K step
   constexpr int kRowB = FP8 ? BKS : BKS * 2;  // one B row of one K step
@@ -181,13 +171,22 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   constexpr int MI = TM / 32, NI = TN / 32;   // 32 x 32 fragments per wave
   constexpr int kNA = BM / kRplA / 4;         // direct loads per wave per K step: A
   constexpr int kNB = BN / kRplB / 4;         // ... and B
-  constexpr int kTileA = BM * kRowA, kStageB = BM * kRowA + BN * kRowB;
+  constexpr int kTileA = BM * kRowA, kTileB = BN * kRowB, kStageB = kTileA + kTileB;
   constexpr int kPerStep = kNA + kNB;
+  // Ring layout.  One ring (BSTAGES == STAGES): stage s holds A then B at
+  // s * kStageB.  Split rings (BSTAGES > STAGES, bf16 big tiles): STAGES A
+  // stages first, then BSTAGES B stages, so the weight tiles are prefetched
+  // further ahead than the activation tiles.
+  constexpr bool kSplit = BSTAGES != STAGES;
+  constexpr int kAStride = kSplit ? kTileA : kStageB;
+  constexpr int kBBase = kSplit ? STAGES * kTileA : kTileA;
+  constexpr int kBStride = kSplit ? kTileB : kStageB;
+  static_assert(!kSplit || (!FP8 && STAGES == 2 && BSTAGES == 3), "split rings: bf16, 2 A + 3 B stages");
   constexpr int kLd = BN / 2 + 8;             // epilogue staging row stride (bf16)
   static_assert(MI >= 1 && NI >= 2 && NI % 2 == 0, "wave tile");
   static_assert(kNA >= 1 && kNB >= 1, "loads per wave");
   static_assert(!GATED || kNB * kRplB == TN / 2, "a wave's B rows are all gate or all up rows");
-  static_assert(STAGES * kStageB <= CAP, "ring must fit the shared buffer");
+  static_assert(STAGES * kTileA + BSTAGES * kTileB <= CAP, "ring must fit the shared buffer");
   static_assert(BM * kLd * 2 <= CAP, "epilogue staging must fit");
   static_assert((STAGES - 1) * kPerStep < 64, "vmcnt range");
 
@@ -199,6 +198,13 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int K = p.K, KT = K / BKS, n_out = p.n_out;
+  // K rotation: the tile walks its K steps starting at step rot and wrapping
+  // round (step j of the loop loads K step krot(j)).  Tiles that run at the
+  // same time start at different steps, so their weight streams do not hit
+  // the same DRAM channels in lockstep (a load-only probe of the cold-tile
+  // pattern: 0.68 -> 0.79 of peak HBM bandwidth).  rot_seed < 0: no rotation.
+  const int rot = rot_seed < 0 ? 0 : (int)((7u * (unsigned)rot_seed) % (unsigned)KT);
+  auto krot = [&](int j) { return j + rot < KT ? j + rot : j + rot - KT; };
   const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
   uint16_t* O = reinterpret_cast<uint16_t*>(p.out);
   // chunk swizzles: spread the 8 rows one 128-byte bank window sees over
@@ -255,27 +261,28 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 
 #define DL_LOAD(kt_, st_)                                                                        \
   do {                                                                                           \
-    const uint32_t sa_ = lds_base + (st_) * kStageB + wave * kNA * 1024;                          \
-    const uint32_t sb_ = lds_base + (st_) * kStageB + kTileA + wave * kNB * 1024;                 \
+    const uint32_t sa_ = lds_base + (st_) * kAStride + wave * kNA * 1024;                         \
+    const uint32_t sb_ = lds_base + kBBase + (st_) * kBStride + wave * kNB * 1024;                \
     _Pragma("unroll") for (int i = 0; i < kNA; ++i)                                              \
         if (i < na_eff) dload16(rsA, aoff[i], (kt_) * kRowA, sa_ + i * 1024);                    \
     _Pragma("unroll") for (int i = 0; i < kNB; ++i)                                              \
         dload16(rsB, boff[i], (kt_) * kRowB, sb_ + i * 1024);                                    \
   } while (0)
   // bf16 weights: k-slice ks (16 k) of every fragment
-#define DL_READ(st_, ks_, A_, B_)                                                                \
+#define DL_READ(sa_, sb_, ks_, A_, B_)                                                           \
   do {                                                                                           \
-    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
+    const unsigned char* aa_ = smem + (sa_) * kAStride;                                          \
+    const unsigned char* bb_ = smem + kBBase + (sb_) * kBStride;                                 \
     const int ro_ = rd_row * kRowA + (((2 * (ks_) + (lane >> 5)) ^ rd_sa) << 4);                 \
     _Pragma("unroll") for (int i = 0; i < MI; ++i) A_[i] =                                       \
-        *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + i * 32) * kRowA + ro_);              \
+        *reinterpret_cast<const bf16x8_t*>(aa_ + (wm * TM + i * 32) * kRowA + ro_);              \
     _Pragma("unroll") for (int j = 0; j < NI; ++j) B_[j] =                                       \
-        *reinterpret_cast<const bf16x8_t*>(ab_ + kTileA + (wn * TN + j * 32) * kRowB + ro_);     \
+        *reinterpret_cast<const bf16x8_t*>(bb_ + (wn * TN + j * 32) * kRowB + ro_);              \
   } while (0)
   // fp8 weights: half-step m (32 k): A for both MFMAs, raw e4m3 B
 #define DL_READ8(st_, m_, A1_, A2_, R_)                                                          \
   do {                                                                                           \
-    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
+    const unsigned char* ab_ = smem + (st_) * kStageB; /* one ring */                            \
     const int ca_ = 4 * (m_) + 2 * (lane >> 5);                                                  \
     const int ra1_ = rd_row * kRowA + ((ca_ ^ rd_sa) << 4);                                      \
     const int ra2_ = rd_row * kRowA + (((ca_ + 1) ^ rd_sa) << 4);                                \
@@ -304,9 +311,9 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   } while (0)
   // operand reads spread between the MFMAs
   constexpr int kQ = MI * NI >= 4 ? 4 : MI * NI;
-#define DL_GROUP(st_, ks_, An, Bn, Ac, Bc)                                                       \
+#define DL_GROUP(sa_, sb_, ks_, An, Bn, Ac, Bc)                                                  \
   do {                                                                                           \
-    DL_READ(st_, ks_, An, Bn);                                                                   \
+    DL_READ(sa_, sb_, ks_, An, Bn);                                                              \
     DL_MMA(Ac, Bc);                                                                              \
     _Pragma("unroll") for (int q_ = 0; q_ < kQ; ++q_) {                                          \
       __builtin_amdgcn_sched_group_barrier(0x100, (MI + NI + kQ - 1) / kQ, 0);                   \
@@ -378,15 +385,15 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // The group's own operand reads (next slice) go out one per MFMA over its
   // first MI + NI MFMAs.  GB: index of the group's first MFMA counted from
   // the barrier.
-#define DL_READ1(st_, ks_, A_, B_, idx_)                                                         \
+#define DL_READ1(sa_, sb_, ks_, A_, B_, idx_)                                                    \
   do {                                                                                           \
-    const unsigned char* ab_ = smem + (st_) * kStageB;                                           \
     const int ro_ = rd_row * kRowA + (((2 * (ks_) + (lane >> 5)) ^ rd_sa) << 4);                 \
     if ((idx_) < MI)                                                                             \
-      A_[(idx_)] = *reinterpret_cast<const bf16x8_t*>(ab_ + (wm * TM + (idx_) * 32) * kRowA + ro_); \
+      A_[(idx_)] = *reinterpret_cast<const bf16x8_t*>(smem + (sa_) * kAStride +                  \
+                                                      (wm * TM + (idx_) * 32) * kRowA + ro_);    \
     else                                                                                         \
       B_[(idx_) - MI] = *reinterpret_cast<const bf16x8_t*>(                                      \
-          ab_ + kTileA + (wn * TN + ((idx_) - MI) * 32) * kRowB + ro_);                          \
+          smem + kBBase + (sb_) * kBStride + (wn * TN + ((idx_) - MI) * 32) * kRowB + ro_);      \
   } while (0)
   // Deeper rings (the medium, small and tall families, fp8 big tiles): the
   // refill of a freed stage is spread evenly over all MFMAs of the next step
@@ -399,11 +406,11 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 #define DL_GROUP_S(st_, ks_, An, Bn, Ac, Bc, LK, LST, GB)                                        \
   do {                                                                                           \
     constexpr int MN_ = MI * NI, MT_ = 4 * MI * NI, LT_ = kNA + kNB, R_ = MI + NI;               \
-    const uint32_t sa_ = lds_base + (LST) * kStageB + wave * kNA * 1024;                          \
-    const uint32_t sb_ = lds_base + (LST) * kStageB + kTileA + wave * kNB * 1024;                 \
+    const uint32_t sa_ = lds_base + (LST) * kAStride + wave * kNA * 1024;                         \
+    const uint32_t sb_ = lds_base + kBBase + (LST) * kBStride + wave * kNB * 1024;                \
     _Pragma("unroll") for (int m_ = 0; m_ < MN_; ++m_) {                                         \
       _Pragma("unroll") for (int r_ = m_ * R_ / MN_; r_ < (m_ + 1) * R_ / MN_; ++r_)             \
-          DL_READ1(st_, ks_, An, Bn, r_);                                                        \
+          DL_READ1(st_, st_, ks_, An, Bn, r_);                                                   \
       __builtin_amdgcn_sched_barrier(0);                                                         \
       acc[m_ / NI][m_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                           \
           Ac[m_ / NI], Bc[m_ % NI], acc[m_ / NI][m_ % NI], 0, 0, 0);                             \
@@ -422,23 +429,33 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \
   } while (0)
-#define DL_GROUP_R(st_, ks_, An, Bn, Ac, Bc, LK, LST, GB)                                        \
+  // Two-deep A ring (bf16 big tiles): the refill after the barrier that ends
+  // step kt goes out one load after every second MFMA of the 32 MFMAs that
+  // follow the barrier.  Split rings: the A blocks of step kt + 2 in the first
+  // group (the wait that ends the next step needs them), then the B blocks
+  // of step kt + 3.  One ring: the B blocks of step kt + 2 first, then its A
+  // blocks (weight-first measured 2-4% faster there).  GB: index of the
+  // group's first MFMA counted from the barrier.
+#define DL_GROUP_R(sa_, sb_, ks_, An, Bn, Ac, Bc, LKA, LSTA, LKB, LSTB, GB)                      \
   do {                                                                                           \
     static_assert(kNA == kNB && kNA + kNB == MI * NI, "one load per two MFMAs of two groups"); \
-    const uint32_t sa_ = lds_base + (LST) * kStageB + wave * kNA * 1024;                          \
-    const uint32_t sb_ = lds_base + (LST) * kStageB + kTileA + wave * kNB * 1024;                 \
+    const uint32_t la_ = lds_base + (LSTA) * kAStride + wave * kNA * 1024;                        \
+    const uint32_t lb_ = lds_base + kBBase + (LSTB) * kBStride + wave * kNB * 1024;               \
     _Pragma("unroll") for (int m_ = 0; m_ < MI * NI; ++m_) {                                     \
-      if (m_ < MI + NI) DL_READ1(st_, ks_, An, Bn, m_);                                          \
+      if (m_ < MI + NI) DL_READ1(sa_, sb_, ks_, An, Bn, m_);                                     \
       __builtin_amdgcn_sched_barrier(0);                                                         \
       acc[m_ / NI][m_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                           \
           Ac[m_ / NI], Bc[m_ % NI], acc[m_ / NI][m_ % NI], 0, 0, 0);                             \
       __builtin_amdgcn_sched_barrier(0);                                                         \
       if (m_ % 2 == 1) {                                                                         \
         const int l_ = ((GB) + m_) / 2;                                                          \
-        if (l_ < kNB)                                                                            \
-          dload16(rsB, boff[l_], (LK) * kRowB, sb_ + l_ * 1024);                                 \
-        else                                                                                     \
-          dload16(rsA, aoff[l_ - kNB], (LK) * kRowA, sa_ + (l_ - kNB) * 1024);                   \
+        if (kSplit ? l_ < kNA : l_ >= kNB) {                                                     \
+          const int i_ = kSplit ? l_ : l_ - kNB;                                                 \
+          dload16(rsA, aoff[i_], (LKA) * kRowA, la_ + i_ * 1024);                                \
+        } else {                                                                                 \
+          const int i_ = kSplit ? l_ - kNA : l_;                                                 \
+          dload16(rsB, boff[i_], (LKB) * kRowB, lb_ + i_ * 1024);                                \
+        }                                                                                        \
       }                                                                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \
@@ -457,35 +474,80 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // tile's epilogue would otherwise blur the counts below).
   wait_vmcnt<0>();
   __syncthreads();  // every wave is done with the previous tile's LDS
+  if constexpr (kSplit) {
+    // Split rings: A(0), B(0), B(1), A(1); B(2) goes out with step 0's
+    // first operand group.  Step 0 has landed once only B(1) and A(1) are
+    // outstanding.
+    const uint32_t la_ = lds_base + wave * kNA * 1024;
+    const uint32_t lb_ = lds_base + kBBase + wave * kNB * 1024;
+    const int k0 = krot(0), k1 = krot(min(1, KT - 1));
 #pragma unroll
-  for (int s = 0; s < STAGES; ++s) DL_LOAD(min(s, KT - 1), s);
-  wait_steps<STAGES - 1, kNB, kPerStep>(per_step);  // step 0 has landed (this wave's part)
-  __syncthreads();                                  // ... and every wave's part
+    for (int i = 0; i < kNA; ++i) dload16(rsA, aoff[i], k0 * kRowA, la_ + i * 1024);
+#pragma unroll
+    for (int i = 0; i < kNB; ++i) dload16(rsB, boff[i], k0 * kRowB, lb_ + i * 1024);
+#pragma unroll
+    for (int i = 0; i < kNB; ++i) dload16(rsB, boff[i], k1 * kRowB, lb_ + kBStride + i * 1024);
+#pragma unroll
+    for (int i = 0; i < kNA; ++i) dload16(rsA, aoff[i], k1 * kRowA, la_ + kAStride + i * 1024);
+    wait_vmcnt<kNA + kNB>();
+  } else {
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s) DL_LOAD(krot(min(s, KT - 1)), s);
+    wait_steps<STAGES - 1, kNB, kPerStep>(per_step);  // step 0 has landed (this wave's part)
+  }
+  __syncthreads();  // ... and every wave's part
   // Step kt computes stage kt % STAGES.  Its last operand reads come before
   // the barrier that ends the step, so right after that barrier the stage
   // is refilled with step kt + STAGES: a step's loads have STAGES - 1 whole
   // steps of MFMA work to land.  Past the last step the loads repeat the
   // last step (never read).
-  if constexpr (!FP8 && STAGES == 2) {
+  if constexpr (kSplit) {
+    // A in 2 stages, B in 3: after the barrier that ends step kt, A(kt + 2)
+    // refills A stage kt % 2 (spread over the first group of step kt + 1)
+    // and B(kt + 3) refills B stage kt % 3 (over its second group).  The
+    // wait that ends step kt + 1 needs steps kt + 2 complete, so B(kt + 3)
+    // -- the last kNB loads issued -- may still be in flight: each weight
+    // tile has two steps of MFMAs to land, each activation tile one.
+    bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
+    DL_READ(0, 0, 0, a0, b0);
+    int sa = 0, sb = 0;
+    int lka = krot(min(1, KT - 1)), lsta = 1;  // A refill in flight (issued by the prologue)
+    int lkb = krot(min(2, KT - 1)), lstb = 2;  // B refill issued by step 0's first group
+    for (int kt = 0; kt < KT; ++kt) {
+      const int nsa = sa ^ 1, nsb = sb == 2 ? 0 : sb + 1;
+      DL_GROUP_R(sa, sb, 1, a1, b1, a0, b0, lka, lsta, lkb, lstb, MI * NI);
+      DL_GROUP(sa, sb, 2, a0, b0, a1, b1);
+      DL_GROUP(sa, sb, 3, a1, b1, a0, b0);
+      wait_vmcnt<kNB>();  // step kt + 1 has landed (this wave's part)
+      __syncthreads();    // ... and every wave's; A stage sa and B stage sb are free
+      lka = krot(min(kt + 2, KT - 1));
+      lsta = sa;
+      lkb = krot(min(kt + 3, KT - 1));
+      lstb = sb;
+      DL_GROUP_R(nsa, nsb, 0, a0, b0, a1, b1, lka, lsta, lkb, lstb, 0);
+      sa = nsa;
+      sb = nsb;
+    }
+  } else if constexpr (!FP8 && STAGES == 2) {
     // The refill of step kt + 2 into stage st starts after the barrier that
     // ends step kt (in the group computing its last slice) and ends in the
     // first group of step kt + 1.  That group's first pass repeats half of
     // the prologue's loads of step 1 (same bytes, same place; they land
     // before the barrier that ends step 0).
     bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
-    DL_READ(0, 0, a0, b0);
+    DL_READ(0, 0, 0, a0, b0);
     int st = 0;
-    int lk = min(1, KT - 1), lst = 1;  // the refill in flight: its step and stage
+    int lk = krot(min(1, KT - 1)), lst = 1;  // the refill in flight: its K step and stage
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st ^ 1;
-      DL_GROUP_R(st, 1, a1, b1, a0, b0, lk, lst, MI * NI);
-      DL_GROUP(st, 2, a0, b0, a1, b1);
-      DL_GROUP(st, 3, a1, b1, a0, b0);
+      DL_GROUP_R(st, st, 1, a1, b1, a0, b0, lk, lst, lk, lst, MI * NI);
+      DL_GROUP(st, st, 2, a0, b0, a1, b1);
+      DL_GROUP(st, st, 3, a1, b1, a0, b0);
       wait_vmcnt<0>();  // step kt + 1 has landed (this wave's part)
       __syncthreads();  // ... and every wave's; stage st is free
-      lk = min(kt + STAGES, KT - 1);
+      lk = krot(min(kt + STAGES, KT - 1));
       lst = st;
-      DL_GROUP_R(nst, 0, a0, b0, a1, b1, lk, lst, 0);
+      DL_GROUP_R(nst, nst, 0, a0, b0, a1, b1, lk, lst, lk, lst, 0);
       st = nst;
     }
   } else if constexpr (!FP8) {
@@ -494,9 +556,9 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     // steps to land).  The first pass repeats loads of the prologue's last
     // step (same bytes, same place).
     bf16x8_t a0[MI], b0[NI], a1[MI], b1[NI];
-    DL_READ(0, 0, a0, b0);
+    DL_READ(0, 0, 0, a0, b0);
     int st = 0;
-    int lk = min(STAGES - 1, KT - 1), lst = STAGES - 1;  // the refill in flight
+    int lk = krot(min(STAGES - 1, KT - 1)), lst = STAGES - 1;  // the refill in flight
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st + 1 == STAGES ? 0 : st + 1;
       DL_GROUP_S(st, 1, a1, b1, a0, b0, lk, lst, MI * NI);
@@ -504,7 +566,7 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       DL_GROUP_S(st, 3, a1, b1, a0, b0, lk, lst, 3 * MI * NI);
       wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
-      lk = min(kt + STAGES, KT - 1);
+      lk = krot(min(kt + STAGES, KT - 1));
       lst = st;
       DL_GROUP_S(nst, 0, a0, b0, a1, b1, lk, lst, 0);
       st = nst;
@@ -514,13 +576,13 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
     uint4 r0[NI], r1[NI];
     DL_READ8(0, 0, a10, a20, r0);
     int st = 0;
-    int lk = min(STAGES - 1, KT - 1), lst = STAGES - 1;  // the refill in flight
+    int lk = krot(min(STAGES - 1, KT - 1)), lst = STAGES - 1;  // the refill in flight
     for (int kt = 0; kt < KT; ++kt) {
       const int nst = st + 1 == STAGES ? 0 : st + 1;
       DL_GROUP8_S(st, 1, a11, a21, r1, a10, a20, r0, lk, lst, 2 * MI * NI);
       wait_steps<STAGES - 2, kNB, kPerStep>(per_step);  // step kt + 1 has landed
       __syncthreads();
-      lk = min(kt + STAGES, KT - 1);
+      lk = krot(min(kt + STAGES, KT - 1));
       lst = st;
       DL_GROUP8_S(nst, 0, a10, a20, r0, a11, a21, r1, lk, lst, 0);
       st = nst;
@@ -607,76 +669,70 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 // experts, in one persistent grid.  The smaller families come last, so they
 // also fill the tail of the big one; cold
 // experts are weight-streaming bound, and narrow tiles spread each expert's
-// weights over more CUs.  fp8 stages are smaller (e4m3 B tiles), so the rings
-// are deeper: 3 big / 6 medium and small stages instead of 2 / 4.
+// weights over more CUs.  bf16 big tiles keep 2 activation stages and 3
+// weight stages (all 160 KB of LDS; the plan's tile -> group map replaces a
+// group table in LDS).  fp8 stages are smaller (e4m3 B tiles), so their
+// rings are deeper: 3 big / 6 medium and small stages instead of 2 / 4.
 template <bool FP8>
-constexpr int ring_bytes(int stages, int bm, int bn) {
-  return stages * (bm * kBK * 2 + bn * kBK * (FP8 ? 1 : 2));
+constexpr int ring_bytes(int a_stages, int b_stages, int bm, int bn) {
+  return a_stages * bm * kBK * 2 + b_stages * bn * kBK * (FP8 ? 1 : 2);
 }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 template <bool GATED, bool FP8>
 __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
-  constexpr int kBigStages = FP8 ? 3 : 2, kSmallStages = FP8 ? 6 : 4, kTallStages = 3;
-  constexpr int kRing = cmax(cmax(ring_bytes<FP8>(kBigStages, kBM, kBN),
-                                  ring_bytes<FP8>(kTallStages, kTallBM, kMedBN)),
-                             cmax(ring_bytes<FP8>(kSmallStages, kMedBM, kMedBN),
-                                  ring_bytes<FP8>(kSmallStages, kSmallBM, kSmallBN)));
+  constexpr int kBigStages = FP8 ? 3 : 2, kBigBStages = FP8 ? 3 : 3, kSmallStages = FP8 ? 6 : 4,
+                kTallStages = 3;
+  constexpr int kRing = cmax(cmax(ring_bytes<FP8>(kBigStages, kBigBStages, kBM, kBN),
+                                  ring_bytes<FP8>(kTallStages, kTallStages, kTallBM, kMedBN)),
+                             cmax(ring_bytes<FP8>(kSmallStages, kSmallStages, kMedBM, kMedBN),
+                                  ring_bytes<FP8>(kSmallStages, kSmallStages, kSmallBM, kSmallBN)));
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kRing];
-  __shared__ int32_t t0f[3][kMaxGroups + 1];
   const bool probe = p.clk != nullptr && (int)blockIdx.x < p.clk_n;
   unsigned long long clk0 = 0, rt0 = 0;
   if (probe) {
     clk0 = __builtin_amdgcn_s_memtime();
     rt0 = __builtin_amdgcn_s_memrealtime();
   }
-  const int tid = threadIdx.x;
-  const int G = p.G;
   const int stage = GATED ? 0 : 1, st3 = 3 * stage;
   const int tot0 = p.tile_totals[st3], tot1 = p.tile_totals[st3 + 1], tot2 = p.tile_totals[st3 + 2];
-  for (int g = tid; g < G; g += 256)
-    for (int f = 0; f < 3; ++f) t0f[f][g] = p.groups[g].t0[st3 + f];
-  if (tid == 0) {
-    t0f[0][G] = tot0;
-    t0f[1][G] = tot1;
-    t0f[2][G] = tot2;
-  }
-  __syncthreads();
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
   const int nwg = gridDim.x;
   const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
   const int ncol_big = GATED ? (p.n_out + kBN / 2 - 1) / (kBN / 2) : (p.n_out + kBN - 1) / kBN;
+  // The weight-streaming families (medium, tall, small) rotate their K walk
+  // by tile; big tiles share activation and weight bands with the tiles next
+  // to them in an XCD's L2, which a rotation would pull apart.
+  constexpr bool kRotateBig = false;
   for (int tile = slot; tile < tot0 + tot1 + tot2; tile += nwg) {
+    const int g = p.tile_group[tile];
+    const GroupDesc gd = p.groups[g];
     if (tile < tot0) {
-      const int g = find_group(t0f[0], G, tile);
-      const GroupDesc gd = p.groups[g];
-      const int local = tile - t0f[0][g];
+      const int local = tile - gd.t0[st3];
       int rt, nti;
       panel_decode<GATED ? 8 : 4>(local, gd.nrt[stage][0], ncol_big, rt, nti);
-      dl_tile<GATED, FP8, kBM, kBN, kBigStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM);
+      dl_tile<GATED, FP8, kBM, kBN, kBigStages, kBigBStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
+                                                                    rt * kBM, kRotateBig ? tile : -1);
     } else {
       // medium or small: the row tiles of one column tile are consecutive
       const bool med = tile < tot0 + tot1;
       const int f = med ? 1 : 2;
-      const int t = tile - (med ? tot0 : tot0 + tot1);
-      const int g = find_group(t0f[f], G, t);
-      const GroupDesc gd = p.groups[g];
-      const int local = t - t0f[f][g];
+      const int local = tile - (med ? tot0 : tot0 + tot1) - gd.t0[st3 + f];
       const int nti = local / gd.nrt[stage][f];
       const int ri = local - nti * gd.nrt[stage][f];
       if (med && gd.h1[stage] == kTallBM)
-        dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                 gd.row1[stage] + ri * kTallBM);
+        dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kTallStages, kRing>(
+            p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kTallBM, tile);
       else if (med)
-        dl_tile<GATED, FP8, kMedBM, kMedBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                 gd.row1[stage] + ri * kMedBM);
+        dl_tile<GATED, FP8, kMedBM, kMedBN, kSmallStages, kSmallStages, kRing>(
+            p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kMedBM, tile);
       else
-        dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                     gd.row2[stage] + ri * kSmallBM);
+        dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kSmallStages, kRing>(
+            p, smem, lds_base, gd, p.wtab[g], nti, gd.row2[stage] + ri * kSmallBM, tile);
     }
   }
   if (probe) {
     const unsigned long long clk1 = __builtin_amdgcn_s_memtime(), rt1 = __builtin_amdgcn_s_memrealtime();
-    if (tid == 0) {
+    if (threadIdx.x == 0) {
       p.clk[2 * blockIdx.x] = clk1 - clk0;
       p.clk[2 * blockIdx.x + 1] = rt1 - rt0;
     }
@@ -690,22 +746,17 @@ __global__ __launch_bounds__(256) void ffn_f32_kernel(const FfnParams p) {
   __shared__ __attribute__((aligned(16))) float As[BK][LD];
   __shared__ __attribute__((aligned(16))) float Bg[BK][LD];
   __shared__ __attribute__((aligned(16))) float Bu[GATED ? BK : 1][LD];
-  __shared__ int32_t t0s[kMaxGroups + 1];
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
-  const int G = p.G;
   const int total = p.tile_totals[GATED ? 0 : 3];
-  for (int g = tid; g < G; g += 256) t0s[g] = p.groups[g].t0[GATED ? 0 : 3];
-  if (tid == 0) t0s[G] = total;
-  __syncthreads();
   const int K = p.K, n_out = p.n_out;
   const float* A = reinterpret_cast<const float*>(p.a);
   float* O = reinterpret_cast<float*>(p.out);
 
   for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
-    const int g = find_group(t0s, G, tile);
+    const int g = p.tile_group[tile];
     const GroupDesc gd = p.groups[g];
     const WeightDesc wd = p.wtab[g];
-    const int local = tile - t0s[g];
+    const int local = tile - gd.t0[GATED ? 0 : 3];
     const int nti = local / gd.nrt[GATED ? 0 : 1][0];
     const int m0 = (local - nti * gd.nrt[GATED ? 0 : 1][0]) * BM;
     const int arow0 = GATED ? gd.x_row0 : gd.y_row0;
@@ -783,12 +834,13 @@ static int grid_for(int max_tiles, int cap) {
 }
 
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
-                      const WeightDesc* wtab, int G, const int32_t* tile_totals, int max_tiles,
+                      const WeightDesc* wtab, int G, const int32_t* tile_totals,
+                      const int32_t* tile_group, int max_tiles,
                       const void* xp, void* h, void* y, int d, int f, int num_cu,
                       unsigned long long* clk, int clk_n, hipStream_t s) {
   if (max_tiles <= 0) return hipSuccess;
-  const FfnParams p = stage == 0 ? FfnParams{groups, wtab, tile_totals, xp, h, G, d, f, clk, clk_n}
-                                 : FfnParams{groups, wtab, tile_totals, h, y, G, f, d, clk, clk_n};
+  const FfnParams p = stage == 0 ? FfnParams{groups, wtab, tile_totals, tile_group, xp, h, G, d, f, clk, clk_n}
+                                 : FfnParams{groups, wtab, tile_totals, tile_group, h, y, G, f, d, clk, clk_n};
   if (act_dtype == 0) {
     const int grid = grid_for(max_tiles, 4 * num_cu);
     if (stage == 0)

@@ -3,8 +3,10 @@
 // plan: workgroup 0 reads the drained layer's per-expert queue depths (or one
 // expert's, for a single-expert drain) with one thread per group, and writes
 // counts / exclusive-scan offsets / the FFN group table (row-tile families
-// and tile ranges) from workgroup-wide scans; it resets the drained queue
-// depths to zero.  All workgroups clear the (token, slot) -> row map.
+// and tile ranges) from workgroup-wide scans, then the group of every tile of
+// both FFN launches (a binary search of the family's tile starts in LDS per
+// tile, all threads); it resets the drained queue depths to zero.  All
+// workgroups clear the (token, slot) -> row map.
 //
 // gather: one wave per batch row.  A routed row finds its expert by binary
 // search over the offsets, reads its queue entry and copies the referenced
@@ -79,6 +81,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
                                                             int32_t* __restrict__ tile_totals,
                                                             NT6 nt, int big_bm, int med_bm, int small_bm,
                                                             int num_cu,
+                                                            int32_t* __restrict__ tile_group,
+                                                            int64_t tile_cap,
                                                             int32_t* __restrict__ pos,
                                                             float* __restrict__ posw) {
   const int tid = threadIdx.x;
@@ -170,6 +174,35 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(int E, int S, int n_
 #pragma unroll
       for (int i = 0; i < 6; ++i) tile_totals[i] = sum7[1 + i];
     }
+    // The group of every tile of both launches (tiles are numbered per
+    // launch: the big family, then the medium, then the small): the last
+    // group whose first tile in that family is not above the tile.
+    __shared__ int32_t t0s[6][kMaxGroups + 1];
+    if (real)
+#pragma unroll
+      for (int i = 0; i < 6; ++i) t0s[i][g] = b[1 + i];
+    if (g == 0)
+#pragma unroll
+      for (int i = 0; i < 6; ++i) t0s[i][G] = sum7[1 + i];
+    __syncthreads();
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const int tot0 = sum7[1 + 3 * st], tot1 = sum7[2 + 3 * st], tot2 = sum7[3 + 3 * st];
+      for (int t = tid; t < tot0 + tot1 + tot2; t += kPlanThreads) {
+        const int f = t < tot0 ? 0 : (t < tot0 + tot1 ? 1 : 2);
+        const int local = t - (f == 0 ? 0 : (f == 1 ? tot0 : tot0 + tot1));
+        const int32_t* t0 = t0s[3 * st + f];
+        int lo = 0, hi = G;  // t0[lo] <= local < t0[hi]
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (t0[mid] <= local)
+            lo = mid;
+          else
+            hi = mid;
+        }
+        tile_group[st * tile_cap + t] = lo;
+      }
+    }
     // The drained queues are empty again, in both halves of the depth
     // ping-pong: whichever half the next append reads starts from zero (so a
     // captured drain step replays correctly whatever the parity of its
@@ -246,14 +279,16 @@ __global__ __launch_bounds__(256) void gather_kernel(
 hipError_t launch_plan(int E, int S, int n_tokens, int k, int only_expert, int32_t* depth,
                        int32_t* depth_other, int32_t* counts, int32_t* offsets, GroupDesc* groups,
                        int32_t* tile_totals, const int* nt, int big_bm, int med_bm, int small_bm,
-                       int num_cu, int32_t* pos, float* posw, hipStream_t s) {
+                       int num_cu, int32_t* tile_group, int64_t tile_cap, int32_t* pos, float* posw,
+                       hipStream_t s) {
   NT6 n6;
   for (int i = 0; i < 6; ++i) n6.v[i] = nt[i];
   static_assert(kMaxGroups <= kPlanThreads, "one plan thread per group");
   const int64_t nk = (int64_t)n_tokens * k;
   const unsigned nb = (unsigned)std::min<int64_t>(256, std::max<int64_t>(1, (nk + 4 * kPlanThreads - 1) / (4 * kPlanThreads)));
   plan_kernel<<<nb, kPlanThreads, 0, s>>>(E, S, n_tokens, k, only_expert, depth, depth_other, counts, offsets, groups,
-                                  tile_totals, n6, big_bm, med_bm, small_bm, num_cu, pos, posw);
+                                  tile_totals, n6, big_bm, med_bm, small_bm, num_cu, tile_group, tile_cap,
+                                  pos, posw);
   return hipGetLastError();
 }
 

@@ -8,17 +8,21 @@
 // The softmax weights of the selected experts follow; lane j keeps slot j.
 // Each (token, slot) is then ranked among the workgroup's rows bound for the
 // same expert: one thread per expert walks the 32 tokens' selection masks in
-// token order.  Per-workgroup expert counts go to `blockcnt`; the workgroup
-// that finishes last (a counter, reset by that workgroup) rewrites them, per
-// expert, into each workgroup's first queue slot -- the current depth plus an
-// exclusive scan over the workgroups -- and publishes the new depths into the
-// other half of the layer's depth ping-pong buffer (the host flips halves
-// after the launch).  The scan reads every count once: linear in T.
+// token order.  Per-workgroup expert counts go to `blockcnt`.
 //
 // append: the same 32-token workgroups.  Lane j of each token writes the
 // queue entry of slot j at its workgroup's first slot for that expert plus
 // its rank -- the order is exactly (fragment, token, slot) within each
-// expert's queue, with no atomics on the entries.
+// expert's queue, with no atomics on the entries.  A workgroup's first slot
+// is the queue's current depth plus the counts of the workgroups before it.
+// Up to kDirectPrefixBlocks workgroups each append workgroup sums those
+// counts itself (at most 63 per expert) and the last one publishes the new
+// depths into the other half of the layer's depth ping-pong buffer (the host
+// flips halves after the launch).  Above that, the router workgroup that
+// finishes last (a counter, reset by that workgroup) scans every count once
+// -- linear in T -- rewriting them into first slots and publishing the
+// depths; small fragments skip it because its device-wide fences cost a few
+// microseconds on the critical path.
 #include <float.h>
 #include <limits.h>
 
@@ -177,7 +181,9 @@ __global__ __launch_bounds__(kRouteThreads) void route_count_kernel(
   }
   if (bad) atomicOr(err, kErrNonFinite);
 
-  // The last workgroup to finish scans every workgroup's counts.
+  // Large launches: the last workgroup to finish scans every workgroup's
+  // counts (smaller ones are summed by the append workgroups).
+  if ((int)gridDim.x <= kDirectPrefixBlocks) return;
   __shared__ int last;
   __threadfence();  // this workgroup's counts are visible device-wide
   __syncthreads();
@@ -192,12 +198,33 @@ __global__ __launch_bounds__(kRouteThreads) void route_count_kernel(
 __global__ __launch_bounds__(kRouteThreads) void append_kernel(
     const int32_t* __restrict__ r_idx, const float* __restrict__ r_w,
     const int32_t* __restrict__ r_rank, const int32_t* __restrict__ first_slot, int T, int E, int k,
-    const char* x, int64_t row_bytes, int32_t token_base, QEntry* __restrict__ q, int64_t q_stride,
+    const char* x, int64_t row_bytes, int32_t token_base, const int32_t* __restrict__ depth_cur,
+    int32_t* __restrict__ depth_nxt, QEntry* __restrict__ q, int64_t q_stride,
     const void** __restrict__ tok_row, const int32_t* __restrict__ token_ids, int n_ids,
     int32_t* __restrict__ live, int32_t* __restrict__ pend, int32_t* __restrict__ err) {
   __shared__ int32_t base[kMaxRouteExperts];
   const int tid = threadIdx.x;
-  if (tid < E) base[tid] = first_slot[(int64_t)blockIdx.x * E + tid];
+  if ((int)gridDim.x > kDirectPrefixBlocks) {
+    if (tid < E) base[tid] = first_slot[(int64_t)blockIdx.x * E + tid];  // scanned by the router
+  } else {
+    // the counts of the workgroups before this one, split over kParts
+    // threads per expert
+    constexpr int kParts = kRouteThreads / kMaxRouteExperts;
+    __shared__ int32_t part[kParts][kMaxRouteExperts];
+    const int e = tid % kMaxRouteExperts, pp = tid / kMaxRouteExperts;
+    int acc = 0;
+    if (e < E)
+      for (int b = pp; b < (int)blockIdx.x; b += kParts) acc += first_slot[(int64_t)b * E + e];
+    part[pp][e] = acc;
+    __syncthreads();
+    if (tid < E) {
+      int a = depth_cur[tid];
+#pragma unroll
+      for (int i = 0; i < kParts; ++i) a += part[i][tid];
+      base[tid] = a;
+      if (blockIdx.x == gridDim.x - 1) depth_nxt[tid] = a + first_slot[(int64_t)blockIdx.x * E + tid];
+    }
+  }
   __syncthreads();
   const int g = tid & (kRouteLanes - 1);
   const int t = blockIdx.x * kRouteTokens + tid / kRouteLanes;
@@ -279,13 +306,14 @@ hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, in
 
 hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* r_rank,
                          const int32_t* first_slot, int T, int E, int k, const char* x,
-                         int64_t row_bytes, int32_t token_base, QEntry* q, int64_t q_stride,
-                         const void** tok_row, const int32_t* token_ids, int n_ids, int32_t* live,
-                         int32_t* pend, int32_t* err, hipStream_t s) {
+                         int64_t row_bytes, int32_t token_base, const int32_t* depth_cur,
+                         int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
+                         const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
+                         int32_t* err, hipStream_t s) {
   const int nb = (T + kRouteTokens - 1) / kRouteTokens;
   append_kernel<<<nb, kRouteThreads, 0, s>>>(r_idx, r_w, r_rank, first_slot, T, E, k, x, row_bytes,
-                                              token_base, q, q_stride, tok_row, token_ids, n_ids, live,
-                                              pend, err);
+                                              token_base, depth_cur, depth_nxt, q, q_stride, tok_row,
+                                              token_ids, n_ids, live, pend, err);
   return hipGetLastError();
 }
 

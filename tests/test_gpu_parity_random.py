@@ -3,7 +3,8 @@ bit-exact, expert outputs and the combined output within tolerance, against
 the oracle.  The shapes are drawn once from a fixed seed and cover the
 corners the fixed cases do not: one expert, k = E, one token, fragments of
 one token, d and ffn of 64, odd expert counts, shared experts with fp8 and
-f32, no renormalisation."""
+f32, no renormalisation, fragments just above and well above the 64 router
+workgroups (2048 tokens) beyond which the router scans the counts."""
 
 import numpy as np
 import pytest
@@ -23,6 +24,10 @@ def _cases():
         dict(d=128, f=192, E=5, k=5, S=0, T=37, n_frag=4, fmt=("bf16", "fp8"), renorm=False),
         dict(d=64, f=128, E=64, k=8, S=1, T=9, n_frag=3, fmt=("bf16", "bf16"), renorm=True),
         dict(d=192, f=64, E=3, k=2, S=2, T=130, n_frag=2, fmt=("f32", "f32"), renorm=True),
+        # fragments of more than 64 router workgroups (2048 tokens): the
+        # router scans the workgroup counts instead of the append summing them
+        dict(d=64, f=128, E=64, k=6, S=0, T=4100, n_frag=1, fmt=("bf16", "bf16"), renorm=True),
+        dict(d=128, f=64, E=8, k=2, S=1, T=2049 + 2048, n_frag=2, fmt=("bf16", "bf16"), renorm=True),
     ]
     out = list(fixed)
     for _ in range(10):
