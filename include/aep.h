@@ -126,13 +126,15 @@ aep_status aep_workspace_size(const aep_ctx* ctx, size_t* bytes);
 /* Bind a caller-allocated device workspace of at least aep_workspace_size
  * bytes, 256-byte aligned, on the current HIP device.  Initialises it on
  * `stream` and waits for that.  Resets every queue.  The workspace holds the
- * mu-queues, weight tables, the batch buffers and the FFN intermediate. */
+ * mu-queues, weight tables, the batch buffers, the FFN intermediate and (bf16
+ * activations) 32 MiB for the split-K partial sums of FFN launches with few
+ * tiles. */
 aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stream);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): bind the
  * library's own static workspace instead of a caller allocation.  The array
- * holds AEP_STATIC_WORKSPACE_BYTES (64 MiB) on every GPU the library runs on,
+ * holds AEP_STATIC_WORKSPACE_BYTES (96 MiB) on every GPU the library runs on,
  * comes with the code object and lives until the process ends; nothing is
  * allocated or freed by this call.  Otherwise as aep_bind_workspace: on the
  * current HIP device, initialised on `stream` (waits for it), every queue
@@ -144,7 +146,7 @@ aep_status aep_bind_workspace(aep_ctx* ctx, void* d_ws, size_t bytes, void* stre
  * calls return AEP_ERR_STATE until it is bound again.  Work that two such
  * contexts enqueue so that it overlaps on the GPU (before the takeover, or
  * on different streams) races and corrupts both. */
-#define AEP_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+#define AEP_STATIC_WORKSPACE_BYTES ((size_t)96 << 20)
 aep_status aep_bind_static_workspace(aep_ctx* ctx, void* stream);
 
 /* Register one expert's weights for a layer (pointers are borrowed and must

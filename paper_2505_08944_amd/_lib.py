@@ -19,7 +19,7 @@ AEP_OK, AEP_ERR_INVALID_ARG, AEP_ERR_CAPACITY, AEP_ERR_EMPTY, AEP_ERR_STATE, AEP
     AEP_ERR_UNSUPPORTED = range(7)
 AEP_F32, AEP_BF16, AEP_FP8_E4M3 = range(3)
 AEP_POLICY_MTFS, AEP_POLICY_FLFS, AEP_POLICY_DEFRAG = range(3)
-AEP_STATIC_WORKSPACE_BYTES = 64 << 20   # include/aep.h
+AEP_STATIC_WORKSPACE_BYTES = 96 << 20   # include/aep.h
 
 STATUS_NAMES = {0: "AEP_OK", 1: "AEP_ERR_INVALID_ARG", 2: "AEP_ERR_CAPACITY", 3: "AEP_ERR_EMPTY",
                 4: "AEP_ERR_STATE", 5: "AEP_ERR_DEVICE", 6: "AEP_ERR_UNSUPPORTED"}

@@ -82,6 +82,18 @@ constexpr int kSmallBN = 128;           // ... x 128 columns (gate/up: 64 featur
 constexpr int kMedBM = 128;             // medium-family tiles: 128 rows ...
 constexpr int kMedBN = 128;             // ... x 128 columns
 constexpr int kTallBM = 256;            // family 1 of a cold batch: 256 rows x kMedBN columns
+// Split-K of an FFN launch with at most half a grid of tiles: up to kMaxSplit
+// pieces of at least kMinSplitSteps K steps each per tile, for launches of at
+// most kSplitCounters tiles; kSplitPartBytes is one piece's partial sums of a
+// big tile (the largest family).
+constexpr int kMaxSplit = 4;
+constexpr int kMinSplitSteps = 8;
+constexpr int kSplitCounters = 1024;
+constexpr int64_t kSplitPartBytes = (int64_t)kBM * kBN * 4;
+// The partial sums' area of a context: 128 big-tile pieces (a launch of 64
+// big tiles splits in 2, one of 128 small tiles in 2, 32 big tiles in 4;
+// the kernel lowers n_split until a launch's pieces fit).
+constexpr int64_t kSplitBytes = 128 * kSplitPartBytes;
 // f32 path
 constexpr int kBM32 = 64;
 constexpr int kBN32 = 64;
@@ -149,12 +161,16 @@ hipError_t launch_pool_release(int act_dtype, float* pool, int32_t* live, int32_
                                void* out, int32_t* ready, int d, hipStream_t s);
 // stage 0: gate/up (xp -> h), stage 1: down (h -> y); max_tiles bounds the
 // stage's tile count (the exact count is on the device); tile_group is that
-// stage's row of the plan's tile -> group map.
+// stage's row of the plan's tile -> group map.  split_slots (split_bytes
+// bytes) holds the split-K partial sums and split_cnt [kSplitCounters] the
+// pieces finished per tile, zero before the launch and left zero (bf16 / fp8
+// weights; split_slots == nullptr: no split).
 // clk != nullptr: workgroup w < clk_n writes its elapsed (s_memtime,
 // s_memrealtime) ticks to clk[2w], clk[2w + 1] (bf16 / fp8 weights only).
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
                       const WeightDesc* wtab, int G, const int32_t* tile_totals,
-                      const int32_t* tile_group, int max_tiles,
+                      const int32_t* tile_group, float* split_slots, int32_t* split_cnt,
+                      int64_t split_bytes, int max_tiles,
                       const void* xp, void* h, void* y, int d, int f, int num_cu,
                       unsigned long long* clk, int clk_n, hipStream_t s);
 hipError_t launch_combine(int act_dtype, const void* y, int64_t N, int n_tokens, int S, int k,

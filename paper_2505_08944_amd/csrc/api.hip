@@ -49,6 +49,9 @@ struct aep_ctx {
   int64_t tile_cap = 0;  // entries per FFN launch in the tile -> group map
   size_t off_xp = 0, off_rowtok = 0, off_roww = 0, off_pos = 0, off_posw = 0, off_h = 0;
   size_t off_pool = 0, off_live = 0, off_pend = 0;  // token pools (cfg.token_pool)
+  // split-K of the FFN launches (bf16 activations): per-tile piece counters
+  // (cleared with the depth counters at binding) and the partial sums
+  size_t off_splitcnt = 0, off_split = 0, split_bytes = 0;
   size_t ws_need = 0;
   char* ws = nullptr;
   bool ws_static = false;   // ws is the library's static workspace (aep_bind_static_workspace)
@@ -150,6 +153,7 @@ bool layout(Ctx& c) {
   };
   c.off_err = take(256);
   c.off_depth = take(sizeof(int32_t) * L * 2 * E);
+  if (g.act_dtype == AEP_BF16) c.off_splitcnt = take(sizeof(int32_t) * kSplitCounters);
   c.off_q = take(sizeof(QEntry) * L * E * T);
   c.off_tokrow = take(sizeof(void*) * L * T);
   c.off_wtab = take(sizeof(WeightDesc) * L * c.G);
@@ -169,6 +173,10 @@ bool layout(Ctx& c) {
   c.off_pos = take(sizeof(int32_t) * N);
   c.off_posw = take(sizeof(float) * N);
   c.off_h = take((size_t)hrows * f * c.esz);
+  if (g.act_dtype == AEP_BF16) {
+    c.split_bytes = kSplitBytes;
+    c.off_split = take(c.split_bytes);
+  }
   if (g.token_pool) {
     c.off_pool = take(sizeof(float) * L * T * d);
     c.off_live = take(sizeof(int32_t) * L * T);
@@ -607,7 +615,9 @@ static aep_status ffn_stage(Ctx* c, const aep_batch* batch, int stage, void* y, 
   if (mt > INT32_MAX || mt > c->tile_cap) return AEP_ERR_UNSUPPORTED;
   return dev(launch_ffn(stage, c->cfg.act_dtype, c->cfg.w_dtype, c->at<GroupDesc>(c->off_groups),
                         c->wtab(batch->layer), c->G, c->at<int32_t>(c->off_tiles),
-                        c->at<int32_t>(c->off_tilegrp) + stage * c->tile_cap, (int)mt,
+                        c->at<int32_t>(c->off_tilegrp) + stage * c->tile_cap,
+                        c->split_bytes ? c->at<float>(c->off_split) : nullptr,
+                        c->split_bytes ? c->at<int32_t>(c->off_splitcnt) : nullptr, (int64_t)c->split_bytes, (int)mt,
                         c->ws + c->off_xp, c->ws + c->off_h, y, c->cfg.d_model, c->cfg.d_ffn, c->num_cu,
                         c->clk, c->clk_n, as_stream(stream)));
 }

@@ -47,6 +47,9 @@ struct FfnParams {
   const WeightDesc* wtab;
   const int32_t* tile_totals;
   const int32_t* tile_group;  // group of each tile of this launch (written by the plan)
+  float* split_slots;         // split-K partial sums (nullptr: no split)
+  int32_t* split_cnt;         // pieces finished per tile (zero between launches)
+  int64_t split_bytes;        // size of split_slots
   const void* a;  // x_perm (gate/up) or h (down)
   void* out;      // h (gate/up) or y (down)
   int G;
@@ -160,7 +163,8 @@ __device__ __forceinline__ void wait_steps(int per) {
 template <bool GATED, bool FP8, int BM, int BN, int STAGES, int BSTAGES, int CAP>
 __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem, uint32_t lds_base,
                                         const GroupDesc& gd, const WeightDesc& wd, int nti, int m0,
-                                        int rot_seed) {
+                                        int rot_seed, int n_split = 1, int piece = 0, float* slot = nullptr,
+                                        int32_t* cnt = nullptr) {
   constexpr int BKS = kBK;
   constexpr int kRowA = BKS * 2;              // 128 bytes: one A row of one K step
   constexpr int kRowB = FP8 ? BKS : BKS * 2;  // one B row of one K step
@@ -197,14 +201,17 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   asm volatile("" : "+v"(tid));
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int K = p.K, KT = K / BKS, n_out = p.n_out;
+  const int K = p.K, KT0 = K / BKS, n_out = p.n_out;
+  // K steps of this work item: all of them, or piece `piece` of n_split
+  // (split-K): steps [k0, k0 + KT).
+  const int k0 = piece * KT0 / n_split, KT = (piece + 1) * KT0 / n_split - k0;
   // K rotation: the tile walks its K steps starting at step rot and wrapping
   // round (step j of the loop loads K step krot(j)).  Tiles that run at the
   // same time start at different steps, so their weight streams do not hit
   // the same DRAM channels in lockstep (a load-only probe of the cold-tile
   // pattern: 0.68 -> 0.79 of peak HBM bandwidth).  rot_seed < 0: no rotation.
   const int rot = rot_seed < 0 ? 0 : (int)((7u * (unsigned)rot_seed) % (unsigned)KT);
-  auto krot = [&](int j) { return j + rot < KT ? j + rot : j + rot - KT; };
+  auto krot = [&](int j) { return k0 + (j + rot < KT ? j + rot : j + rot - KT); };
   const uint16_t* A = reinterpret_cast<const uint16_t*>(p.a);
   uint16_t* O = reinterpret_cast<uint16_t*>(p.out);
   // chunk swizzles: spread the 8 rows one 128-byte bank window sees over
@@ -600,6 +607,40 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 #undef DL_READ
 #undef DL_LOAD
 
+  // Split-K: every piece stores its f32 partial sums in its part of the
+  // tile's slot, then counts itself finished; the piece that counts last
+  // adds the parts in piece order -- the same order whichever piece that is,
+  // so results are reproducible run to run -- and runs the epilogue.  Parts
+  // and counter are accessed with agent-scope atomics, which are coherent
+  // across the XCDs' L2 caches, and each wave's stores have completed
+  // (vmcnt 0) before the count: no device-wide fence, whose L2 write-back
+  // measured far slower.
+  if (n_split > 1) {
+    // part layout [wave][fragment][register][lane]: 16 stores 256 bytes apart
+    constexpr int kPart = BM * BN;  // floats
+    float* mine = slot + (int64_t)piece * kPart + wave * (MI * NI * 16 * 64) + lane;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        float* dst = mine + (i * NI + j) * (16 * 64);
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          __hip_atomic_store(dst + r * 64, acc[i][j][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    wait_vmcnt<0>();  // every store of this wave has completed
+    __syncthreads();  // ... of every wave; the ring is free
+    volatile int* flag = reinterpret_cast<volatile int*>(smem);
+    if (tid == 0)
+      flag[0] = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n_split - 1;
+    __syncthreads();
+    const bool last = flag[0] != 0;
+    __syncthreads();  // the flag is read before the epilogue reuses the LDS
+    if (!last) return;
+    if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);  // next launch
+  }
+
   // Epilogue: stage bf16 results in LDS ([BM][BN/2 + 8]) and write 16-byte
   // chunks of whole rows.  Gate/up: one pass, feature fragment j pairs with
   // up fragment j + NI/2.  Down: two passes of BN/2 columns (each wave
@@ -631,16 +672,44 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
       }
 #pragma unroll
       for (int i = 0; i < MI; ++i) {
+        // the fragment's values (and its up partner's): the accumulators, or
+        // for a split tile the sum of its pieces' parts in piece order
+        float f0[16], f1[GATED ? 16 : 1];
+        if (n_split > 1) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) f0[r] = 0.f;
+#pragma unroll
+          for (int r = 0; r < (GATED ? 16 : 1); ++r) f1[r] = 0.f;
+          const float* pp = slot + wave * (MI * NI * 16 * 64) + lane;
+          for (int q = 0; q < n_split; ++q) {
+            float* p0 = const_cast<float*>(pp) + (int64_t)q * (BM * BN) + (i * NI + j) * (16 * 64);
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              f0[r] += __hip_atomic_load(p0 + r * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if constexpr (GATED) {
+              float* p1 = p0 + (NI / 2) * (16 * 64);
+#pragma unroll
+              for (int r = 0; r < 16; ++r)
+                f1[r] += __hip_atomic_load(p1 + r * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) f0[r] = acc[i][j][r];
+          if constexpr (GATED)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) f1[r] = acc[i][j + NI / 2][r];
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int rl = wm * TM + i * 32 + c_row(lane, r);
           float v;
           if constexpr (GATED) {
-            const float gv = FP8 ? acc[i][j][r] * sg : acc[i][j][r];
-            const float uv = FP8 ? acc[i][j + NI / 2][r] * su : acc[i][j + NI / 2][r];
+            const float gv = FP8 ? f0[r] * sg : f0[r];
+            const float uv = FP8 ? f1[r] * su : f1[r];
             v = gv * __builtin_amdgcn_rcpf(1.f + __expf(-gv)) * uv;
           } else {
-            v = FP8 ? acc[i][j][r] * sg : acc[i][j][r];
+            v = FP8 ? f0[r] * sg : f0[r];
           }
           Cs[rl * kLd + cl] = (uint16_t)f32_to_bf16_rne(v);
         }
@@ -697,21 +766,50 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   const int tot0 = p.tile_totals[st3], tot1 = p.tile_totals[st3 + 1], tot2 = p.tile_totals[st3 + 2];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_vptr)smem;
   const int nwg = gridDim.x;
-  const int slot = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
   const int ncol_big = GATED ? (p.n_out + kBN / 2 - 1) / (kBN / 2) : (p.n_out + kBN - 1) / kBN;
   // The weight-streaming families (medium, tall, small) rotate their K walk
   // by tile; big tiles share activation and weight bands with the tiles next
   // to them in an XCD's L2, which a rotation would pull apart.
   constexpr bool kRotateBig = false;
-  for (int tile = slot; tile < tot0 + tot1 + tot2; tile += nwg) {
+  const int total = tot0 + tot1 + tot2;
+  // Split-K: a launch of at most half a grid of tiles cuts each tile into
+  // n_split pieces of consecutive K steps (at least kMinSplitSteps each), so
+  // that more CUs stream its weights; the partial sums of a tile's pieces
+  // take n_split parts of its slot (big tiles first, then family 1, then
+  // small, each slot sized for its family).
+  int n_split = 1;
+  int64_t slot1 = 0, slot2 = 0;  // float offsets of the family 1 and small slots
+  if (p.split_slots != nullptr && total > 0 && 2 * total <= nwg && total <= kSplitCounters) {
+    n_split = max(1, min(min(kMaxSplit, nwg / total), p.K / (kBK * kMinSplitSteps)));
+    const int64_t per = (int64_t)tot0 * (kBM * kBN) + (int64_t)tot1 * (kTallBM * kMedBN) +
+                        (int64_t)tot2 * (kSmallBM * kSmallBN);  // floats per piece
+    while (n_split > 1 && (int64_t)n_split * per * 4 > p.split_bytes) --n_split;
+    slot1 = (int64_t)n_split * tot0 * (kBM * kBN);
+    slot2 = slot1 + (int64_t)n_split * tot1 * (kTallBM * kMedBN);
+  }
+  const int items = total * n_split;  // work item = tile * n_split + piece
+  // Work items go round by round: a full round of the grid gives each XCD
+  // (the hardware deals workgroups round robin over the 8 XCDs) a run of
+  // nwg / 8 consecutive items; a partial round gives each XCD a run of
+  // ceil(count / 8), so a launch with fewer items than workgroups still
+  // uses every XCD's L2 and memory path.
+  const int xcd = blockIdx.x & 7, xj = blockIdx.x >> 3;
+  for (int base = 0; base < items; base += nwg) {
+    const int cnt = min(nwg, items - base);
+    const int q = cnt == nwg ? (nwg >> 3) : ((cnt + 7) >> 3);
+    const int idx = xcd * q + xj;
+    if (xj >= q || idx >= cnt) continue;
+    const int item = base + idx;
+    const int tile = item / n_split, piece = item - tile * n_split;
     const int g = p.tile_group[tile];
     const GroupDesc gd = p.groups[g];
     if (tile < tot0) {
       const int local = tile - gd.t0[st3];
       int rt, nti;
       panel_decode<GATED ? 8 : 4>(local, gd.nrt[stage][0], ncol_big, rt, nti);
-      dl_tile<GATED, FP8, kBM, kBN, kBigStages, kBigBStages, kRing>(p, smem, lds_base, gd, p.wtab[g], nti,
-                                                                    rt * kBM, kRotateBig ? tile : -1);
+      dl_tile<GATED, FP8, kBM, kBN, kBigStages, kBigBStages, kRing>(
+          p, smem, lds_base, gd, p.wtab[g], nti, rt * kBM, kRotateBig ? tile : -1, n_split, piece,
+          n_split > 1 ? p.split_slots + (int64_t)tile * n_split * (kBM * kBN) : nullptr, p.split_cnt + tile);
     } else {
       // medium or small: the row tiles of one column tile are consecutive
       const bool med = tile < tot0 + tot1;
@@ -719,15 +817,21 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const int local = tile - (med ? tot0 : tot0 + tot1) - gd.t0[st3 + f];
       const int nti = local / gd.nrt[stage][f];
       const int ri = local - nti * gd.nrt[stage][f];
+      float* sl = n_split == 1 ? nullptr
+                  : med ? p.split_slots + slot1 + (int64_t)(tile - tot0) * n_split * (kTallBM * kMedBN)
+                        : p.split_slots + slot2 + (int64_t)(tile - tot0 - tot1) * n_split * (kSmallBM * kSmallBN);
       if (med && gd.h1[stage] == kTallBM)
         dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kTallStages, kRing>(
-            p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kTallBM, tile);
+            p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kTallBM, tile, n_split, piece, sl,
+            p.split_cnt + tile);
       else if (med)
         dl_tile<GATED, FP8, kMedBM, kMedBN, kSmallStages, kSmallStages, kRing>(
-            p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kMedBM, tile);
+            p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kMedBM, tile, n_split, piece, sl,
+            p.split_cnt + tile);
       else
         dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kSmallStages, kRing>(
-            p, smem, lds_base, gd, p.wtab[g], nti, gd.row2[stage] + ri * kSmallBM, tile);
+            p, smem, lds_base, gd, p.wtab[g], nti, gd.row2[stage] + ri * kSmallBM, tile, n_split, piece, sl,
+            p.split_cnt + tile);
     }
   }
   if (probe) {
@@ -835,12 +939,15 @@ static int grid_for(int max_tiles, int cap) {
 
 hipError_t launch_ffn(int stage, int act_dtype, int w_dtype, const GroupDesc* groups,
                       const WeightDesc* wtab, int G, const int32_t* tile_totals,
-                      const int32_t* tile_group, int max_tiles,
+                      const int32_t* tile_group, float* split_slots, int32_t* split_cnt,
+                      int64_t split_bytes, int max_tiles,
                       const void* xp, void* h, void* y, int d, int f, int num_cu,
                       unsigned long long* clk, int clk_n, hipStream_t s) {
   if (max_tiles <= 0) return hipSuccess;
-  const FfnParams p = stage == 0 ? FfnParams{groups, wtab, tile_totals, tile_group, xp, h, G, d, f, clk, clk_n}
-                                 : FfnParams{groups, wtab, tile_totals, tile_group, h, y, G, f, d, clk, clk_n};
+  const FfnParams p = stage == 0 ? FfnParams{groups, wtab, tile_totals, tile_group, split_slots, split_cnt,
+                                             split_bytes, xp, h, G, d, f, clk, clk_n}
+                                 : FfnParams{groups, wtab, tile_totals, tile_group, split_slots, split_cnt,
+                                             split_bytes, h, y, G, f, d, clk, clk_n};
   if (act_dtype == 0) {
     const int grid = grid_for(max_tiles, 4 * num_cu);
     if (stage == 0)

@@ -85,3 +85,63 @@ def test_tile_families_match_oracle(kind, wdt):
     ctx.release(b)
     ctx.sync()
     del ctx, dev_w, keep
+
+
+# Split-K: a launch of at most half a grid of tiles cuts every tile into
+# n_split = min(4, grid / tiles, K / 512) pieces of consecutive K steps (the
+# slot area permitting); the last piece to finish adds the pieces' f32
+# partial sums in piece order.  Each case below puts at most 128 tiles into
+# at least one launch with K >= 1024, on the families named.
+SPLIT_CASES = {
+    # 2 experts x 16 rows, small tiles: gate/up 32 tiles in 4 pieces, down 32 in 2
+    "small": ([16, 16], 2048, 1024),
+    # medium (100 rows) and tall (200 rows) tiles of a cold batch, 4 pieces
+    "medium_tall": ([100, 200], 2048, 1024),
+    # one 256-row expert: 16 big gate/up tiles in 2 pieces, 4 big down tiles in 4
+    "big": ([256], 1024, 2048),
+    # every family in one launch (big + medium, small, tall; an empty expert):
+    # 56 gate/up and 28 down tiles, 2 pieces each
+    "mixed": ([356, 30, 0, 200], 1024, 1024),
+    # 100 big gate/up tiles (f = 12800): 2 pieces would need 50 MB of partial
+    # sums, more than the 32 MB area, so that launch is not split; the down
+    # launch (4 big tiles, K = 12800) is, in 4 pieces
+    "area_cap": ([256], 1024, 12800),
+}
+
+
+@pytest.mark.parametrize("kind,wdt", [("small", "bf16"), ("small", "fp8"), ("medium_tall", "bf16"),
+                                      ("medium_tall", "fp8"), ("big", "bf16"), ("big", "fp8"),
+                                      ("mixed", "bf16"), ("area_cap", "bf16")])
+def test_split_k_matches_oracle(kind, wdt):
+    """Every element of y against the oracle, and a second run of the same
+    batch bit-identical (the pieces are added in a fixed order, whichever
+    finishes last)."""
+    depths, d, f = SPLIT_CASES[kind]
+    w = synth.Workload(f"split_{kind}_{wdt}", 111, d=d, f=f, E=len(depths), k=1, zipf_s=1.0, mode="rows",
+                       depth_max=max(depths), wdt=wdt)
+    N, per = _rows(w, depths, 21)
+    log(f"case split {kind}/{wdt}: depths {depths}, d={d} f={f}")
+    ws = synth.all_expert_weights(w, 0, threads=4)
+    ctx = make_context(w, max_tokens=N)
+    dev_w = upload_weights(ctx, w, 0, ws)
+    lq = oracle.LayerQueues(w.E, 1)
+    keep = []
+    for e, ex in enumerate(per):
+        if depths[e] == 0:
+            continue
+        t = (to_dev(ex["x"], "bf16"), to_dev(ex["token_ids"], "i32"), to_dev(ex["gate_w"], "f32"))
+        keep.append((e, t))
+        lq.enqueue_rows(e, ex["x"], ex["token_ids"], ex["gate_w"], N)
+    ys = []
+    for rep in range(2):
+        for e, t in keep:
+            ctx.enqueue_rows(0, e, *t, N)
+        b = ctx.rebatch(0)
+        ys.append(to_host(ctx.expert_ffn(b)))
+        ctx.release(b)
+    ctx.sync()
+    ref = oracle.moe_layer(lq, ws, "bf16", wdt)
+    st = assert_close(oracle.bf16_to_f64(ys[0]), ref["y"], BF16_RTOL, f"split {kind}/{wdt} y")
+    assert np.array_equal(ys[0], ys[1]), "split-K results differ between runs"
+    log(f"case split {kind}/{wdt}: y {st}, bit-identical rerun")
+    del ctx, dev_w, keep
