@@ -476,10 +476,11 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Nothing of this wave may still be in flight when the ring is refilled
-  // (the wait counter is in issue order, so earlier stores of the previous
-  // tile's epilogue would otherwise blur the counts below).
-  wait_vmcnt<0>();
+  // The previous tile's epilogue stores may still be in flight: the ring
+  // waits below count this tile's loads only, and since loads complete in
+  // issue order, older outstanding stores can only make those waits
+  // stricter (not waiting for the stores here: fine-grained layer gate/up
+  // -3%).
   __syncthreads();  // every wave is done with the previous tile's LDS
   if constexpr (kSplit) {
     // Split rings: A(0), B(0), B(1), A(1); B(2) goes out with step 0's
