@@ -2,7 +2,8 @@
 (nothing allocated by the binding) computes what a context on a caller-
 allocated workspace computes.
 
-Two bindings in a row on the same GPU, the second with a smaller layer: each
+Bindings in a row on the same GPU, the second with a smaller layer, the
+third one whose FFN launches are split along K: each
 static-workspace layer (route, re-batch, FFN, combine) is compared bit for bit
 with the same layer on a torch-allocated workspace (same kernels, same
 inputs) and within tolerance with the oracle.  The second binding takes the
@@ -52,6 +53,10 @@ def test_static_workspace_matches_allocated_workspace():
     cases = [
         synth.Workload("static_a", 501, d=512, f=1024, E=8, k=2, S=1, zipf_s=1.2, tokens=(700,), n_frag=3),
         synth.Workload("static_b", 502, d=256, f=384, E=16, k=4, zipf_s=1.1, wdt="fp8", tokens=(90,), n_frag=2),
+        # 2 experts, 32 tokens, top-1: 32 small tiles per FFN launch with K of
+        # 2048 and 1024, so both launches are split along K and their piece
+        # counters live in the static array
+        synth.Workload("static_c", 504, d=2048, f=1024, E=2, k=1, zipf_s=1.0, tokens=(32,), n_frag=1),
     ]
     first = None
     for w in cases:
