@@ -246,8 +246,8 @@ def main():
         print(json.dumps({"cold": cold_measurements(args), "fig3_sweep": fig3_sweep()}), flush=True)
         return
     if args.gpus != 1:
-        sys.stderr.write("bench.py measures one GPU: this build has no multi-GPU path (expert-parallel "
-                         "sharding is described in DESIGN.md); run with --gpus 1.\n")
+        sys.stderr.write("bench.py measures one GPU: the library has no multi-GPU path (experts would "
+                         "shard across GPUs by expert parallelism); run with --gpus 1.\n")
         sys.exit(2)
 
     import torch
