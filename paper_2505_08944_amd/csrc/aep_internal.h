@@ -79,6 +79,7 @@ constexpr int kBN = 256;
 constexpr int kBK = 64;
 constexpr int kSmallBM = 64;            // small-family tiles: 64 rows ...
 constexpr int kSmallBN = 128;           // ... x 128 columns (gate/up: 64 features)
+constexpr int kSmallBN8 = 256;          // ... x 256 columns with fp8 weights
 constexpr int kMedBM = 128;             // medium-family tiles: 128 rows ...
 constexpr int kMedBN = 128;             // ... x 128 columns
 constexpr int kTallBM = 256;            // family 1 of a cold batch: 256 rows x kMedBN columns

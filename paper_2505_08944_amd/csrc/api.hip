@@ -102,7 +102,8 @@ using Ctx = aep_ctx;
 // Tiling of the FFN launches: nt[6] = column tiles per row tile, index
 // stage * 3 + family (stage 0 gate/up, 1 down; family big, medium, small),
 // and the row-tile heights.  f32 uses 64 x 64 tiles only; bf16 and fp8
-// weights use 256 x 256 big tiles, 128 x 128 medium and 64 x 128 small ones.
+// weights use 256 x 256 big tiles, 128 x 128 medium and 64 x 128 small ones
+// (64 x 256 with fp8 weights).
 void tiling(const Ctx& c, int nt[6], int* big_bm, int* med_bm, int* small_bm) {
   const int d = c.cfg.d_model, f = c.cfg.d_ffn;
   auto cdiv = [](int a, int b) { return (a + b - 1) / b; };
@@ -114,10 +115,11 @@ void tiling(const Ctx& c, int nt[6], int* big_bm, int* med_bm, int* small_bm) {
   } else {
     nt[0] = cdiv(f, kBN / 2);
     nt[1] = cdiv(f, kMedBN / 2);
-    nt[2] = cdiv(f, kSmallBN / 2);
+    const int sbn = c.cfg.w_dtype == AEP_FP8_E4M3 ? kSmallBN8 : kSmallBN;
+    nt[2] = cdiv(f, sbn / 2);
     nt[3] = cdiv(d, kBN);
     nt[4] = cdiv(d, kMedBN);
-    nt[5] = cdiv(d, kSmallBN);
+    nt[5] = cdiv(d, sbn);
     *big_bm = kBM;
     *med_bm = kMedBM;
     *small_bm = kSmallBM;

@@ -9,8 +9,9 @@
 // blocks of an expert (and for a remainder above 128 rows, unless that would
 // start another round of the grid in a short stage), then 128 x 128 medium
 // tiles (256 x 128 tall ones for a cold batch's remainders above 128 rows)
-// and 64 x 128 small tiles for the ragged row tails and cold experts.  One
-// launch covers a whole skewed batch, from a 1-row expert to the hottest one:
+// and 64 x 128 small tiles (64 x 256 with fp8 weights) for the ragged row
+// tails and cold experts.  One launch covers a whole skewed batch, from a
+// 1-row expert to the hottest one:
 // every big tile first, then the smaller ones, which also fill the tail of
 // the big family.  The workgroup -> tile map is XCD aware: hardware
 // dispatches workgroups round robin over the 8 XCDs, so workgroup w works on
@@ -677,21 +678,38 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
         // for a split tile the sum of its pieces' parts in piece order
         float f0[16], f1[GATED ? 16 : 1];
         if (n_split > 1) {
+          // every piece's part of the fragment (and of its partner) is
+          // loaded before any is added: one memory round trip, not one per
+          // piece; then the sum in piece order
+          float t0[kMaxSplit][16], t1[kMaxSplit][GATED ? 16 : 1];
+          float* pp = slot + wave * (MI * NI * 16 * 64) + lane + (i * NI + j) * (16 * 64);
+#pragma unroll
+          for (int q = 0; q < kMaxSplit; ++q) {
+            if (q < n_split) {
+              float* p0 = pp + (int64_t)q * (BM * BN);
+#pragma unroll
+              for (int r = 0; r < 16; ++r)
+                t0[q][r] = __hip_atomic_load(p0 + r * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              if constexpr (GATED) {
+                float* p1 = p0 + (NI / 2) * (16 * 64);
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                  t1[q][r] = __hip_atomic_load(p1 + r * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              }
+            }
+          }
 #pragma unroll
           for (int r = 0; r < 16; ++r) f0[r] = 0.f;
 #pragma unroll
           for (int r = 0; r < (GATED ? 16 : 1); ++r) f1[r] = 0.f;
-          const float* pp = slot + wave * (MI * NI * 16 * 64) + lane;
-          for (int q = 0; q < n_split; ++q) {
-            float* p0 = const_cast<float*>(pp) + (int64_t)q * (BM * BN) + (i * NI + j) * (16 * 64);
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              f0[r] += __hip_atomic_load(p0 + r * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if constexpr (GATED) {
-              float* p1 = p0 + (NI / 2) * (16 * 64);
+          for (int q = 0; q < kMaxSplit; ++q) {
+            if (q < n_split) {
 #pragma unroll
-              for (int r = 0; r < 16; ++r)
-                f1[r] += __hip_atomic_load(p1 + r * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              for (int r = 0; r < 16; ++r) f0[r] += t0[q][r];
+              if constexpr (GATED)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) f1[r] += t1[q][r];
             }
           }
         } else {
@@ -750,12 +768,15 @@ constexpr int ring_bytes(int a_stages, int b_stages, int bm, int bn) {
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 template <bool GATED, bool FP8>
 __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
+  // fp8 small tiles are twice as wide: per K step they read as many weight
+  // bytes as bf16 ones and half the activation bytes per weight byte
+  constexpr int kSBN = FP8 ? kSmallBN8 : kSmallBN;
   constexpr int kBigStages = FP8 ? 3 : 2, kBigBStages = FP8 ? 3 : 3, kSmallStages = FP8 ? 6 : 4,
                 kTallStages = 3;
   constexpr int kRing = cmax(cmax(ring_bytes<FP8>(kBigStages, kBigBStages, kBM, kBN),
                                   ring_bytes<FP8>(kTallStages, kTallStages, kTallBM, kMedBN)),
                              cmax(ring_bytes<FP8>(kSmallStages, kSmallStages, kMedBM, kMedBN),
-                                  ring_bytes<FP8>(kSmallStages, kSmallStages, kSmallBM, kSmallBN)));
+                                  ring_bytes<FP8>(kSmallStages, kSmallStages, kSmallBM, kSBN)));
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kRing];
   const bool probe = p.clk != nullptr && (int)blockIdx.x < p.clk_n;
   unsigned long long clk0 = 0, rt0 = 0;
@@ -783,7 +804,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
   if (p.split_slots != nullptr && total > 0 && 2 * total <= nwg && total <= kSplitCounters) {
     n_split = max(1, min(min(kMaxSplit, nwg / total), p.K / (kBK * kMinSplitSteps)));
     const int64_t per = (int64_t)tot0 * (kBM * kBN) + (int64_t)tot1 * (kTallBM * kMedBN) +
-                        (int64_t)tot2 * (kSmallBM * kSmallBN);  // floats per piece
+                        (int64_t)tot2 * (kSmallBM * kSBN);  // floats per piece
     while (n_split > 1 && (int64_t)n_split * per * 4 > p.split_bytes) --n_split;
     slot1 = (int64_t)n_split * tot0 * (kBM * kBN);
     slot2 = slot1 + (int64_t)n_split * tot1 * (kTallBM * kMedBN);
@@ -820,7 +841,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
       const int ri = local - nti * gd.nrt[stage][f];
       float* sl = n_split == 1 ? nullptr
                   : med ? p.split_slots + slot1 + (int64_t)(tile - tot0) * n_split * (kTallBM * kMedBN)
-                        : p.split_slots + slot2 + (int64_t)(tile - tot0 - tot1) * n_split * (kSmallBM * kSmallBN);
+                        : p.split_slots + slot2 + (int64_t)(tile - tot0 - tot1) * n_split * (kSmallBM * kSBN);
       if (med && gd.h1[stage] == kTallBM)
         dl_tile<GATED, FP8, kTallBM, kMedBN, kTallStages, kTallStages, kRing>(
             p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kTallBM, tile, n_split, piece, sl,
@@ -830,7 +851,7 @@ __global__ __launch_bounds__(256, 1) void ffn_dlds_kernel(const FfnParams p) {
             p, smem, lds_base, gd, p.wtab[g], nti, gd.row1[stage] + ri * kMedBM, tile, n_split, piece, sl,
             p.split_cnt + tile);
       else
-        dl_tile<GATED, FP8, kSmallBM, kSmallBN, kSmallStages, kSmallStages, kRing>(
+        dl_tile<GATED, FP8, kSmallBM, kSBN, kSmallStages, kSmallStages, kRing>(
             p, smem, lds_base, gd, p.wtab[g], nti, gd.row2[stage] + ri * kSmallBM, tile, n_split, piece, sl,
             p.split_cnt + tile);
     }
