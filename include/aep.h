@@ -302,7 +302,11 @@ aep_status aep_rebatch(aep_ctx* ctx, int32_t layer, aep_batch* out, void* stream
 /* Expert FFN of a batch: every group g computes, on its rows,
  * y = W_down (silu(W_gate x) * (W_up x)), silu(v) = v / (1 + e^-v), with
  * f32 accumulation; the intermediate h is rounded to the act dtype.
- * y: device [n_rows][d] act dtype, caller-owned. */
+ * y: device [n_rows][d] act dtype, caller-owned.  A launch with few tiles
+ * (bf16 and fp8 weights) splits its reduction into pieces whose f32 partial
+ * sums are added in a fixed order, so results are reproducible run to run;
+ * its per-tile counters live in the workspace, so FFN launches of one
+ * context must not overlap on the GPU (issue them in stream order). */
 aep_status aep_expert_ffn(aep_ctx* ctx, const aep_batch* batch, void* y, void* stream);
 
 /* The two halves of aep_expert_ffn, for callers that schedule (or time) them
