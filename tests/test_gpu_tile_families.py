@@ -111,7 +111,7 @@ SPLIT_CASES = {
 
 @pytest.mark.parametrize("kind,wdt", [("small", "bf16"), ("small", "fp8"), ("medium_tall", "bf16"),
                                       ("medium_tall", "fp8"), ("big", "bf16"), ("big", "fp8"),
-                                      ("mixed", "bf16"), ("area_cap", "bf16")])
+                                      ("mixed", "bf16"), ("mixed", "fp8"), ("area_cap", "bf16")])
 def test_split_k_matches_oracle(kind, wdt):
     """Every element of y against the oracle, and a second run of the same
     batch bit-identical (the pieces are added in a fixed order, whichever
