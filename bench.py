@@ -427,6 +427,16 @@ def main():
     # ---------------------------------------------------------------- CPU oracle
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens, args.cpu_budget_s)
+        if args.workload == "c2":
+            # the same oracle on two more of the workloads, bounded samples
+            # (context for the main value; about 12 s more of host time)
+            others = {}
+            for name, n_tok, budget in (("c1", 0, 2.0), ("c3", 512, 5.0)):
+                ow = synth.workload(name)
+                r = cpu_baseline(ow, n_tok, budget)
+                others[name] = {"workload": ow.description or name, "value": r["value"], "unit": r["unit"],
+                                "sample": r["sample"]}
+            res["cpu_baseline"]["other_workloads"] = others
 
     print(json.dumps(res), flush=True)
 
