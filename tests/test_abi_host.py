@@ -117,3 +117,29 @@ def test_workspace_accounting_and_unbound_state():
     finally:
         assert lib.aep_destroy(h) == 0
     assert lib.aep_destroy(None) == 0
+
+
+def test_static_workspace_capacity():
+    """The static workspace (AEP_STATIC_WORKSPACE_BYTES) holds a Mixtral-shaped
+    layer (d=4096, ffn=14336, 8 experts, top-2, bf16) with 900 queued tokens,
+    the split-K partial sums included, and not one with 1000; an f32 layer has
+    no split-K area (its launches are never split)."""
+    L, lib = _lib()
+
+    def need(**kw):
+        st, h = _create(L, lib, **kw)
+        assert st == 0, (kw, st)
+        n = ctypes.c_size_t()
+        assert lib.aep_workspace_size(h, ctypes.byref(n)) == 0
+        lib.aep_destroy(h)
+        return n.value
+
+    mix = dict(n_layers=1, d_model=4096, d_ffn=14336)
+    assert need(max_tokens_per_layer=900, **mix) <= L.AEP_STATIC_WORKSPACE_BYTES
+    assert need(max_tokens_per_layer=1000, **mix) > L.AEP_STATIC_WORKSPACE_BYTES
+    small = dict(n_layers=1, d_model=256, d_ffn=512, max_tokens_per_layer=64)
+    bf16 = need(**small)
+    f32 = need(act_dtype=L.AEP_F32, w_dtype=L.AEP_F32, **small)
+    # a tiny bf16 layer's workspace is mostly its 32 MiB of partial sums; the
+    # f32 one has none
+    assert bf16 >= 32 << 20 and f32 < 4 << 20, (bf16, f32)
