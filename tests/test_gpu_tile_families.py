@@ -145,3 +145,46 @@ def test_split_k_matches_oracle(kind, wdt):
     assert np.array_equal(ys[0], ys[1]), "split-K results differ between runs"
     log(f"case split {kind}/{wdt}: y {st}, bit-identical rerun")
     del ctx, dev_w, keep
+
+
+# Expert shapes of the weight-streaming sweep at their real sizes (the bench
+# runs more experts of each): same-shape experts of n rows each.  Mixtral
+# shape, 4 x 16 rows: 448 small gate/up tiles, and a down launch of 128 small
+# tiles (K = 14336) split in 2; EP-share shape with fp8 weights, 12 x 64
+# rows: 192 wide (64 x 256) small tiles per launch, not split; and, smaller
+# than any sweep shape so that its fp8 weights quantise in seconds, a long-K
+# fp8 down launch of 16 wide tiles (K = 4096) split in 4.
+SWEEP_CASES = {
+    "d4096_f14336_bf16_n16": (4, 16, 4096, 14336, "bf16"),
+    "d4096_f2048_fp8_n64": (12, 64, 4096, 2048, "fp8"),
+    "d2048_f4096_fp8_n64": (2, 64, 2048, 4096, "fp8"),
+}
+
+
+@pytest.mark.parametrize("case", sorted(SWEEP_CASES))
+def test_sweep_shapes_match_oracle(case):
+    """Every element of y against the oracle at the sweep's expert shapes."""
+    G, n, d, f, wdt = SWEEP_CASES[case]
+    depths = [n] * G
+    w = synth.Workload(f"sweep_{case}", 113, d=d, f=f, E=G, k=1, zipf_s=1.0, mode="rows", depth_max=n,
+                       wdt=wdt)
+    N, per = _rows(w, depths, 23)
+    log(f"case sweep {case}: {G} experts x {n} rows, d={d} f={f} {wdt}")
+    ws = synth.all_expert_weights(w, 0, threads=8)
+    ctx = make_context(w, max_tokens=N)
+    dev_w = upload_weights(ctx, w, 0, ws)
+    lq = oracle.LayerQueues(w.E, 1)
+    keep = []
+    for e, ex in enumerate(per):
+        t = (to_dev(ex["x"], "bf16"), to_dev(ex["token_ids"], "i32"), to_dev(ex["gate_w"], "f32"))
+        keep.append(t)
+        ctx.enqueue_rows(0, e, *t, N)
+        lq.enqueue_rows(e, ex["x"], ex["token_ids"], ex["gate_w"], N)
+    b = ctx.rebatch(0)
+    y = to_host(ctx.expert_ffn(b))
+    ctx.release(b)
+    ctx.sync()
+    ref = oracle.moe_layer(lq, ws, "bf16", wdt)
+    st = assert_close(oracle.bf16_to_f64(y), ref["y"], BF16_RTOL, f"sweep {case} y")
+    log(f"case sweep {case}: y {st}")
+    del ctx, dev_w, keep, ws
