@@ -612,11 +612,17 @@ __device__ __forceinline__ void dl_tile(const FfnParams& p, unsigned char* smem,
   // Split-K: every piece stores its f32 partial sums in its part of the
   // tile's slot, then counts itself finished; the piece that counts last
   // adds the parts in piece order -- the same order whichever piece that is,
-  // so results are reproducible run to run -- and runs the epilogue.  Parts
-  // and counter are accessed with agent-scope atomics, which are coherent
-  // across the XCDs' L2 caches, and each wave's stores have completed
-  // (vmcnt 0) before the count: no device-wide fence, whose L2 write-back
-  // measured far slower.
+  // so results are reproducible run to run -- and runs the epilogue.
+  // Ordering: parts and counter are accessed only with agent-scope atomics,
+  // which the hardware performs at the level that is coherent across the
+  // XCDs' L2 caches; every wave waits for its part stores to be acknowledged
+  // (vmcnt 0) and the workgroup barrier orders that before the counter
+  // increment; the finisher issues its part loads only after the increment
+  // that returned n_split - 1 (the result reaches them through LDS and a
+  // barrier).  So each part is complete at the coherent level before any
+  // load of it is issued.  The atomics are relaxed (no release/acquire
+  // fences): at agent scope those write back and invalidate the whole L2,
+  // which made the pieces slower than no split.
   if (n_split > 1) {
     // part layout [wave][fragment][register][lane]: 16 stores 256 bytes apart
     constexpr int kPart = BM * BN;  // floats
