@@ -423,6 +423,7 @@ def main():
     if not args.no_cold and not args.step_only:
         res["cold"] = cold_measurements(args)
         res["fig3_sweep"] = fig3_sweep()
+        res["ep_share_layer"] = {wdt: ep_share_layer(wdt) for wdt in ("bf16", "fp8")}
 
     # ---------------------------------------------------------------- CPU oracle
     if not args.no_cpu_baseline:
@@ -511,6 +512,98 @@ def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0, flush="read"):
     del ctx, W, rows, flush_buf
     torch.cuda.empty_cache()
     return t, byts, 6.0 * d * f * N
+
+
+def ep_share_layer(wdt: str, steps: int = 20, warmup: int = 3):
+    """One GPU's expert-parallel share as a whole layer: the 16 resident
+    experts' queues (Zipf depths 4096 ... 111 rows) enqueued as explicit
+    rows, re-batched and run through both FFN launches, steps back to back on
+    one stream; rows/s = routed rows / time per step."""
+    import synth
+    import torch
+    import paper_2505_08944_amd as aep
+    dev = torch.device("cuda", 0)
+    w4 = synth.workload("c4")
+    groups = [int(n) for n in synth.rows_workload(w4)["depths"].tolist()]
+    d, f, E, N = w4.d, w4.f, len(groups), int(sum(groups))
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+    ctx = aep.Context(1, E, d, f, 1, wdt=wdt, max_tokens_per_layer=N)
+    W = []
+    for e in range(E):
+        if wdt == "fp8":
+            mats = [torch.randint(0, 126, s, generator=g, device=dev, dtype=torch.uint8)
+                    for s in [(f, d), (f, d), (d, f)]]
+            sc = [torch.full((2 * f,), 1.0, dtype=torch.bfloat16, device=dev) * 0.001,
+                  torch.full((d,), 1.0, dtype=torch.bfloat16, device=dev) * 0.001]
+        else:
+            mats = [(torch.randn(s, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+                    for s in [(f, d), (f, d), (d, f)]]
+            sc = [None, None]
+        ctx.set_expert_weights(0, e, *mats, *sc)
+        W.append(mats + sc)
+    rows = [torch.randn((n, d), generator=g, device=dev).to(torch.bfloat16) for n in groups]
+    tok = torch.arange(N, dtype=torch.int32, device=dev)
+    gw = torch.ones(N, dtype=torch.float32, device=dev)
+    y = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
+
+    def step():
+        o = 0
+        for e, n in enumerate(groups):
+            ctx.enqueue_rows(0, e, rows[e], tok[o:o + n], gw[o:o + n], N)
+            o += n
+        b = ctx.rebatch(0)
+        ctx.expert_ffn(b, y[:b.n_rows])
+        ctx.release(b)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ctx.sync()
+    t = e0.elapsed_time(e1) / 1e3 / steps
+    fl = 6.0 * d * f * N
+    del ctx, W, rows, y
+    torch.cuda.empty_cache()
+    return {"experts": E, "rows": N, "weights": wdt, "ms_per_step": round(t * 1e3, 4),
+            "rows_per_s": round(N / t, 1), "tflops": round(fl / t / 1e12, 1),
+            "mfma_frac": round(fl / t / 1e12 / PEAK_BF16_TFLOPS, 4), "steps": steps}
+
+
+def stream_reference():
+    """The achievable-bandwidth reference beside the cold fractions: torch's
+    own copy kernel over 1 GiB on this GPU (bytes read + written), caches
+    flushed first (median of 5)."""
+    import torch
+    dev = torch.device("cuda", 0)
+    n = 1 << 30
+    src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    flush_buf = torch.empty(n, dtype=torch.uint8, device=dev)
+    res = {}
+    for name, fn, moved in (("copy", lambda: dst.copy_(src), 2 * n),):
+        fn()
+        ts = []
+        for _ in range(5):
+            _flush(flush_buf, "read")
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        gbs = moved / float(np.median(ts)) / 1e9
+        res[f"{name}_GBps"] = round(gbs, 1)
+        res[f"{name}_frac"] = round(gbs / PEAK_HBM_GBS, 4)
+    res["note"] = "torch copy_ of 1 GiB (bytes read + written), caches flushed"
+    del src, dst, flush_buf
+    torch.cuda.empty_cache()
+    return res
 
 
 def hot_measurements(c2_hot_rows: int, drain_hot_rows: int):
@@ -644,6 +737,7 @@ def cold_measurements(args):
         out[f"ep_share_d4096_f2048_{wdt}"] = {"experts": len(cold4), "rows": sum(cold4), "ms": round(t * 1e3, 4),
                                              "GBps": round(byts / t / 1e9, 1),
                                              "hbm_frac": round(byts / t / 1e9 / PEAK_HBM_GBS, 4), "bytes": byts}
+    out["stream_reference"] = stream_reference()
     return out
 
 
