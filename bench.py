@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=0,
                     help="tokens of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ep-layer", choices=["bf16", "fp8"], default=None,
+                    help="only the EP share as a whole layer (16 experts, rows mode), with these weights")
     ap.add_argument("--threads", type=int, default=min(16, os.cpu_count() or 1),
                     help="host threads for input generation")
     ap.add_argument("--no-cold", action="store_true",
@@ -241,6 +243,9 @@ def main():
         return
     if args.cold_case:
         print(json.dumps({"cold_case": cold_case(args.cold_case)}), flush=True)
+        return
+    if args.ep_layer:
+        print(json.dumps({"ep_share_layer": ep_share_layer(args.ep_layer)}), flush=True)
         return
     if args.cold_only:
         print(json.dumps({"cold": cold_measurements(args), "fig3_sweep": fig3_sweep()}), flush=True)
@@ -517,8 +522,9 @@ def time_rows_ffn(groups, d, f, wdt, reps=5, seed=0, flush="read"):
 def ep_share_layer(wdt: str, steps: int = 20, warmup: int = 3):
     """One GPU's expert-parallel share as a whole layer: the 16 resident
     experts' queues (Zipf depths 4096 ... 111 rows) enqueued as explicit
-    rows, re-batched and run through both FFN launches, steps back to back on
-    one stream; rows/s = routed rows / time per step."""
+    rows in one grouped call (one receive buffer, rows grouped by expert),
+    re-batched and run through both FFN launches, steps back to back on one
+    stream; rows/s = routed rows / time per step."""
     import synth
     import torch
     import paper_2505_08944_amd as aep
@@ -542,16 +548,13 @@ def ep_share_layer(wdt: str, steps: int = 20, warmup: int = 3):
             sc = [None, None]
         ctx.set_expert_weights(0, e, *mats, *sc)
         W.append(mats + sc)
-    rows = [torch.randn((n, d), generator=g, device=dev).to(torch.bfloat16) for n in groups]
+    rows = torch.randn((N, d), generator=g, device=dev).to(torch.bfloat16)
     tok = torch.arange(N, dtype=torch.int32, device=dev)
     gw = torch.ones(N, dtype=torch.float32, device=dev)
     y = torch.empty((N, d), dtype=torch.bfloat16, device=dev)
 
     def step():
-        o = 0
-        for e, n in enumerate(groups):
-            ctx.enqueue_rows(0, e, rows[e], tok[o:o + n], gw[o:o + n], N)
-            o += n
+        ctx.enqueue_rows_grouped(0, groups, rows, tok, gw, N)
         b = ctx.rebatch(0)
         ctx.expert_ffn(b, y[:b.n_rows])
         ctx.release(b)

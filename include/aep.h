@@ -185,6 +185,19 @@ aep_status aep_enqueue_rows(aep_ctx* ctx, int32_t layer, int32_t expert, const v
                             const int32_t* token_ids, const int32_t* slots, const float* gate_w,
                             int32_t n, int32_t n_tokens, void* stream);
 
+/* Receptor for rows of several experts at once (e.g. one expert-parallel
+ * receive buffer): rows [n][d] act dtype, grouped by expert in ascending
+ * expert order, h_counts[e] (host, E entries, >= 0) of them for expert e,
+ * n = sum of h_counts; token_ids, slots (NULL: all 0) and gate_w [n] as in
+ * aep_enqueue_rows.  The queues end up exactly as after aep_enqueue_rows for
+ * each expert in ascending order, in one launch.  The count prefix is copied
+ * to the workspace from host memory (hipMemcpyAsync), so the call is not
+ * meant for graph capture.  AEP_ERR_CAPACITY (nothing changed) if any
+ * expert's queue or the layer would overflow; n == 0 is a no-op. */
+aep_status aep_enqueue_rows_grouped(aep_ctx* ctx, int32_t layer, const int32_t* h_counts, const void* rows,
+                                    const int32_t* token_ids, const int32_t* slots, const float* gate_w,
+                                    int32_t n_tokens, void* stream);
+
 /* Host-side queue totals of a layer (no device access). */
 aep_status aep_queue_depth(const aep_ctx* ctx, int32_t layer, int64_t* tokens, int64_t* rows);
 

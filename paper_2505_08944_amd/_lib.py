@@ -80,6 +80,7 @@ _SIG = {
     "aep_set_expert_weights": (ctypes.c_int, [_P, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "aep_route_enqueue": (ctypes.c_int, [_P, _I32, _P, _P, _I32, _P, _P, _P]),
     "aep_enqueue_rows": (ctypes.c_int, [_P, _I32, _I32, _P, _P, _P, _P, _I32, _I32, _P]),
+    "aep_enqueue_rows_grouped": (ctypes.c_int, [_P, _I32, _P, _P, _P, _P, _P, _I32, _P]),
     "aep_queue_depth": (ctypes.c_int, [_P, _I32, ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
     "aep_expert_counts": (ctypes.c_int, [_P, _I32, _P, _P]),
     "aep_pick_layer": (ctypes.c_int, [_P, _I32, ctypes.c_double, _I32, ctypes.POINTER(_I32)]),

@@ -201,6 +201,27 @@ class Context:
         if n:
             self._frag_refs[layer].extend([rows, token_ids, gate_w] + ([slots] if slots is not None else []))
 
+    def enqueue_rows_grouped(self, layer: int, counts, rows: torch.Tensor, token_ids: torch.Tensor,
+                             gate_w: torch.Tensor, n_tokens: int, slots: Optional[torch.Tensor] = None) -> None:
+        """Rows of several experts in one call: rows grouped by expert in
+        ascending order, counts[e] of them for expert e (host sequence)."""
+        h = np.ascontiguousarray(np.asarray(counts, dtype=np.int32))
+        if h.shape != (self.n_experts,):
+            raise ValueError(f"counts: expected {self.n_experts} entries, got {h.shape}")
+        n = rows.shape[0]
+        _need(rows, "rows", self.act_torch, (n, self.d_model))
+        _need(token_ids, "token_ids", torch.int32, (n,))
+        _need(gate_w, "gate_w", torch.float32, (n,))
+        if slots is not None:
+            _need(slots, "slots", torch.int32, (n,))
+        if int(h.sum()) != n:
+            raise ValueError(f"counts sum to {int(h.sum())}, rows has {n}")
+        L.check(self.lib.aep_enqueue_rows_grouped(self.h, layer, h.ctypes.data, rows.data_ptr(),
+                                                  token_ids.data_ptr(), _ptr(slots), gate_w.data_ptr(), n_tokens,
+                                                  _stream()), "aep_enqueue_rows_grouped")
+        if n:
+            self._frag_refs[layer].extend([rows, token_ids, gate_w] + ([slots] if slots is not None else []))
+
     def queue_depth(self, layer: int) -> Tuple[int, int]:
         t, r = ctypes.c_int64(), ctypes.c_int64()
         L.check(self.lib.aep_queue_depth(self.h, layer, ctypes.byref(t), ctypes.byref(r)), "aep_queue_depth")

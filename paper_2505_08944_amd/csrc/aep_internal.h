@@ -125,6 +125,12 @@ hipError_t launch_append(const int32_t* r_idx, const float* r_w, const int32_t* 
                          int32_t* depth_nxt, QEntry* q, int64_t q_stride, const void** tok_row,
                          const int32_t* token_ids, int n_ids, int32_t* live, int32_t* pend,
                          int32_t* err, hipStream_t s);
+// Rows of several experts in one launch: rows [pre[e], pre[e+1]) to queue e
+// (pre: device, E + 1 entries, exclusive prefix of the per-expert counts).
+hipError_t launch_enqueue_grouped(const char* rows, int64_t row_bytes, const int32_t* token_ids,
+                                  const int32_t* slots, const float* gate_w, int n, int n_tokens, int k, int E,
+                                  const int32_t* pre, const int32_t* depth_cur, int32_t* depth_nxt, QEntry* q,
+                                  int64_t q_stride, int32_t* err, hipStream_t s);
 hipError_t launch_enqueue_rows(const char* rows, int64_t row_bytes, const int32_t* token_ids,
                                const int32_t* slots, const float* gate_w, int n, int n_tokens,
                                int k, int expert, int E, const int32_t* depth_cur,

@@ -52,6 +52,7 @@ struct aep_ctx {
   // split-K of the FFN launches (bf16 activations): per-tile piece counters
   // (cleared with the depth counters at binding) and the partial sums
   size_t off_splitcnt = 0, off_split = 0, split_bytes = 0;
+  size_t off_grppre = 0;  // aep_enqueue_rows_grouped: prefix of the per-expert counts
   size_t ws_need = 0;
   char* ws = nullptr;
   bool ws_static = false;   // ws is the library's static workspace (aep_bind_static_workspace)
@@ -156,6 +157,7 @@ bool layout(Ctx& c) {
   c.off_err = take(256);
   c.off_depth = take(sizeof(int32_t) * L * 2 * E);
   if (g.act_dtype == AEP_BF16) c.off_splitcnt = take(sizeof(int32_t) * kSplitCounters);
+  c.off_grppre = take(sizeof(int32_t) * (E + 1));
   c.off_q = take(sizeof(QEntry) * L * E * T);
   c.off_tokrow = take(sizeof(void*) * L * T);
   c.off_wtab = take(sizeof(WeightDesc) * L * c.G);
@@ -468,6 +470,47 @@ aep_status aep_enqueue_rows(aep_ctx* ctx, int32_t layer, int32_t expert, const v
   L.tokens = std::max(L.tokens, n_tokens);
   L.rows += n;
   L.bound[expert] += n;
+  return AEP_OK;
+}
+
+aep_status aep_enqueue_rows_grouped(aep_ctx* ctx, int32_t layer, const int32_t* h_counts, const void* rows,
+                                    const int32_t* token_ids, const int32_t* slots, const float* gate_w,
+                                    int32_t n_tokens, void* stream) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !h_counts) return AEP_ERR_INVALID_ARG;
+  if (!ws_bound(c)) return AEP_ERR_STATE;
+  if (layer < 0 || layer >= c->cfg.n_layers) return AEP_ERR_INVALID_ARG;
+  if (c->cfg.n_shared > 0) return AEP_ERR_UNSUPPORTED;
+  const int E = c->cfg.n_experts;
+  std::vector<int32_t> pre(E + 1, 0);
+  int64_t total = 0;
+  for (int e = 0; e < E; ++e) {
+    if (h_counts[e] < 0) return AEP_ERR_INVALID_ARG;
+    total += h_counts[e];
+    if (total > INT32_MAX) return AEP_ERR_CAPACITY;
+    pre[e + 1] = (int32_t)total;
+  }
+  LayerState& L = c->layers[layer];
+  if (L.rows > 0 && L.pool) return AEP_ERR_STATE;
+  if (total == 0) return AEP_OK;
+  if (!rows || !token_ids || !gate_w || n_tokens < 1) return AEP_ERR_INVALID_ARG;
+  if ((int64_t)n_tokens > c->tmax() || L.rows + total > c->row_cap()) return AEP_ERR_CAPACITY;
+  for (int e = 0; e < E; ++e)
+    if (L.bound[e] + h_counts[e] > c->tmax()) return AEP_ERR_CAPACITY;
+  hipStream_t s = as_stream(stream);
+  int32_t* dpre = c->at<int32_t>(c->off_grppre);
+  if (hipMemcpyAsync(dpre, pre.data(), sizeof(int32_t) * (E + 1), hipMemcpyHostToDevice, s) != hipSuccess)
+    return AEP_ERR_DEVICE;
+  const int64_t row_bytes = (int64_t)c->cfg.d_model * c->esz;
+  hipError_t e = launch_enqueue_grouped(reinterpret_cast<const char*>(rows), row_bytes, token_ids, slots, gate_w,
+                                        (int)total, n_tokens, c->cfg.top_k, E, dpre, c->depth(layer, L.cur),
+                                        c->depth(layer, L.cur ^ 1), c->q(layer), c->tmax(), c->err(), s);
+  if (e != hipSuccess) return AEP_ERR_DEVICE;
+  L.cur ^= 1;
+  L.pool = false;
+  L.tokens = std::max(L.tokens, n_tokens);
+  L.rows += total;
+  for (int ex = 0; ex < E; ++ex) L.bound[ex] += h_counts[ex];
   return AEP_OK;
 }
 

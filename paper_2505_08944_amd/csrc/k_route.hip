@@ -284,6 +284,59 @@ __global__ __launch_bounds__(256) void enqueue_rows_kernel(
   q[(int64_t)expert * q_stride + depth_cur[expert] + i] = en;
 }
 
+// Rows of several experts in one launch: rows [pre[e], pre[e+1]) go to
+// queue e (pre is the exclusive prefix of the per-expert counts, E + 1
+// entries), each expert's rows in order -- the entries one enqueue_rows
+// launch per expert, experts in ascending order, would write.
+__global__ __launch_bounds__(256) void enqueue_grouped_kernel(
+    const char* rows, int64_t row_bytes, const int32_t* __restrict__ token_ids,
+    const int32_t* __restrict__ slots, const float* __restrict__ gate_w, int n, int n_tokens, int k, int E,
+    const int32_t* __restrict__ pre, const int32_t* __restrict__ depth_cur, int32_t* __restrict__ depth_nxt,
+    QEntry* __restrict__ q, int64_t q_stride, int32_t* __restrict__ err) {
+  __shared__ int32_t sp[kMaxGroups + 1];
+  for (int e = threadIdx.x; e <= E; e += blockDim.x) sp[e] = pre[e];
+  __syncthreads();
+  if (blockIdx.x == 0)
+    for (int e = threadIdx.x; e < E; e += blockDim.x) depth_nxt[e] = depth_cur[e] + (sp[e + 1] - sp[e]);
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int lo = 0, hi = E;  // sp[lo] <= i < sp[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (sp[mid] <= i)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  int tok = token_ids[i];
+  int s = slots ? slots[i] : 0;
+  int flag = 0;
+  if (tok < 0 || tok >= n_tokens) {
+    flag |= kErrTokenRange;
+    tok = 0;
+  }
+  if (s < 0 || s >= k) {
+    flag |= kErrSlotRange;
+    s = 0;
+  }
+  if (flag) atomicOr(err, flag);
+  QEntry en;
+  en.row = rows + (int64_t)i * row_bytes;
+  en.token_slot = tok | (s << kTokenBits);
+  en.w = gate_w[i];
+  q[(int64_t)lo * q_stride + depth_cur[lo] + (i - sp[lo])] = en;
+}
+
+hipError_t launch_enqueue_grouped(const char* rows, int64_t row_bytes, const int32_t* token_ids,
+                                  const int32_t* slots, const float* gate_w, int n, int n_tokens, int k, int E,
+                                  const int32_t* pre, const int32_t* depth_cur, int32_t* depth_nxt, QEntry* q,
+                                  int64_t q_stride, int32_t* err, hipStream_t s) {
+  const int nb = (n + 255) / 256;
+  enqueue_grouped_kernel<<<nb, 256, 0, s>>>(rows, row_bytes, token_ids, slots, gate_w, n, n_tokens, k, E, pre,
+                                             depth_cur, depth_nxt, q, q_stride, err);
+  return hipGetLastError();
+}
+
 hipError_t launch_route(const float* logits, int T, int E, int k, int renorm, int32_t* r_idx,
                         float* r_w, int32_t* r_rank, int32_t* blockcnt, int32_t* idx_out,
                         float* w_out, const int32_t* depth_cur, int32_t* depth_nxt, int32_t* done,

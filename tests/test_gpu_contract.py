@@ -15,7 +15,9 @@ the router on inputs the workload generators do not produce.
   and re-batches bit-exactly (routing against the oracle's route; counts,
   offsets and row order against histogram, cumulative sum and stable sort of
   the flattened expert ids, the textbook routines that pin the oracle's
-  queues), and its outputs agree on sampled tokens.
+  queues), and its outputs agree on sampled tokens;
+* rows of several experts enqueued in one call leave the queues exactly as
+  one call per expert does.
 """
 
 import ctypes
@@ -263,3 +265,62 @@ def test_largest_fragment():
     ctx.sync()
     del ctx, dev, x, lg, y, out
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("wdt", ["bf16", "fp8"])
+def test_grouped_enqueue_equals_per_expert_enqueues(wdt):
+    """aep_enqueue_rows_grouped leaves the queues exactly as aep_enqueue_rows
+    once per expert in ascending order: the same counts, the same gathered
+    rows and the same FFN output bit for bit (empty experts included), and
+    both against the oracle.  A grouped call one row past an expert's
+    capacity returns AEP_ERR_CAPACITY and changes nothing."""
+    depths = [300, 0, 17, 129, 64, 1, 0, 250]
+    w = synth.Workload(f"grouped_{wdt}", 402, d=256, f=512, E=len(depths), k=1, zipf_s=1.0, mode="rows",
+                       depth_max=max(depths), wdt=wdt)
+    g = np.random.default_rng(7)
+    N = int(sum(depths))
+    x = synth.round_to_bf16_bits(g.standard_normal((N, w.d), dtype=np.float32))
+    tok = g.permutation(N).astype(np.int32)
+    gw = g.random(N, dtype=np.float32)
+    ws = synth.all_expert_weights(w, 0, threads=4)
+    xd, td, gd = to_dev(x, "bf16"), to_dev(tok, "i32"), to_dev(gw, "f32")
+    log(f"case grouped {wdt}: depths {depths}")
+    results = []
+    for grouped in (False, True):
+        ctx = make_context(w, max_tokens=N)
+        dev_w = upload_weights(ctx, w, 0, ws)
+        if grouped:
+            # one row past expert 3's capacity: refused, nothing changes
+            over = list(depths)
+            over[3] = ctx.max_tokens + 1  # an expert's queue holds at most max_tokens rows
+            before = (ctx.queue_depth(0), ctx.expert_counts(0).tolist())
+            xo = torch.zeros((sum(over), w.d), dtype=torch.bfloat16, device="cuda")
+            to_ = torch.zeros(sum(over), dtype=torch.int32, device="cuda")
+            go = torch.zeros(sum(over), dtype=torch.float32, device="cuda")
+            assert _status(ctx.enqueue_rows_grouped, 0, over, xo, to_, go, N) == L.AEP_ERR_CAPACITY
+            assert (ctx.queue_depth(0), ctx.expert_counts(0).tolist()) == before
+            ctx.enqueue_rows_grouped(0, depths, xd, td, gd, N)
+        else:
+            o = 0
+            for e, n in enumerate(depths):
+                ctx.enqueue_rows(0, e, xd[o:o + n], td[o:o + n], gd[o:o + n], N)
+                o += n
+        assert ctx.expert_counts(0).tolist() == depths
+        b = ctx.rebatch(0)
+        xp = to_host(b.x_perm())
+        y = to_host(ctx.expert_ffn(b))
+        ctx.release(b)
+        ctx.sync()
+        results.append((xp, y))
+        del ctx, dev_w
+    assert np.array_equal(results[0][0], results[1][0]), "gathered rows differ"
+    assert np.array_equal(results[0][1], results[1][1]), "FFN outputs differ"
+    lq = oracle.LayerQueues(w.E, 1)
+    o = 0
+    for e, n in enumerate(depths):
+        if n:
+            lq.enqueue_rows(e, x[o:o + n], tok[o:o + n], gw[o:o + n], N)
+        o += n
+    ref = oracle.moe_layer(lq, ws, "bf16", wdt)
+    st = assert_close(oracle.bf16_to_f64(results[1][1]), ref["y"], BF16_RTOL, f"grouped {wdt} y")
+    log(f"case grouped {wdt}: bit-identical to per-expert enqueues; y {st}")
